@@ -1,0 +1,51 @@
+"""Determinism and shape checks of the seeded input generators (no method arithmetic)."""
+import json
+import os
+
+import numpy as np
+
+import gcn_synth as gs
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def test_golden_digests():
+    from golden.make_synth_hashes import cases
+    want = json.load(open(os.path.join(HERE, "golden", "synth_hashes.json")))
+    got = dict(cases())
+    assert got == want
+
+
+def test_counter_access_is_random_access():
+    a = gs.draws(0, 7, 0, 5000)
+    b = gs.draws(0, 7, 1234, 100)
+    assert (a[1234:1334] == b).all()
+    assert not (gs.draws(0, 8, 0, 100) == a[:100]).any()
+    # rows regenerated on demand equal the full matrix
+    X = gs.features_normal(50, 33, seed=0, stream=3)
+    np.testing.assert_array_equal(gs.features_normal(50, 33, seed=0, stream=3, row0=17, rows=9), X[17:26])
+    Y = gs.features_bernoulli(40, 70, 0.2, binary=False)
+    np.testing.assert_array_equal(gs.features_bernoulli(40, 70, 0.2, binary=False, row0=5, rows=3), Y[5:8])
+
+
+def test_chung_lu_shape():
+    s, d = gs.chung_lu(3000, 20000)
+    assert s.size == 20000 and (s != d).all()
+    keys = np.minimum(s, d).astype(np.int64) * 3000 + np.maximum(s, d)
+    assert np.unique(keys).size == 20000
+    assert s.min() >= 0 and max(s.max(), d.max()) < 3000
+
+
+def test_feature_statistics():
+    X = gs.features_bernoulli(2000, 500, 0.013)
+    p = (X != 0).mean()
+    sigma = np.sqrt(0.013 * 0.987 / X.size)
+    assert abs(p - 0.013) < 4 * sigma
+    assert set(np.unique(X).tolist()) <= {0.0, 1.0}
+    Z = gs.features_bernoulli(1000, 400, 0.1, binary=False)
+    nz = Z[Z != 0]
+    assert nz.min() > 0 and nz.max() <= 1.0
+    N = gs.features_normal(400, 500)
+    assert abs(N.mean()) < 0.01 and abs(N.std() - 1) < 0.01
+    y = gs.labels(10000, 7)
+    assert y.min() == 0 and y.max() == 6
