@@ -1,0 +1,535 @@
+// api.hip -- the extern "C" entry points declared in include/gcn.h.
+//
+// Every entry point validates its arguments on the host, plans its workspace
+// with the same code for the size query and the real call, and enqueues
+// kernels from the other translation units.  Nothing here allocates device
+// memory.
+#include <string>
+
+#include "internal.h"
+
+namespace gcn {
+
+namespace {
+thread_local std::string g_err;
+}
+
+gcn_status fail(gcn_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+gcn_status hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return GCN_E_HIP;
+}
+
+namespace {
+
+// Workspace protocol: NULL buffer -> report size; else check it is large enough.
+gcn_status ws_protocol(void* d_ws, size_t* ws_bytes, size_t need, const char* who, bool* query) {
+  if (!ws_bytes) return fail(GCN_E_INVALID, std::string(who) + ": ws_bytes is NULL");
+  if (!d_ws) {
+    *ws_bytes = need;
+    *query = true;
+    return GCN_OK;
+  }
+  *query = false;
+  if (*ws_bytes < need)
+    return fail(GCN_E_CAPACITY, std::string(who) + ": workspace of " + std::to_string(*ws_bytes) +
+                                    " bytes, " + std::to_string(need) + " needed");
+  return GCN_OK;
+}
+
+gcn_status check_graph(const gcn_graph* g, const char* who) {
+  if (!g) return fail(GCN_E_INVALID, std::string(who) + ": graph is NULL");
+  if (g->n < 0) return fail(GCN_E_INVALID, std::string(who) + ": negative node count");
+  if (g->n > 0 && (!g->row_ptr || !g->col_idx || !g->dinv))
+    return fail(GCN_E_INVALID, std::string(who) + ": graph arrays missing");
+  return GCN_OK;
+}
+
+gcn_status check_layer(const gcn_layer* L, const char* who) {
+  if (!L) return fail(GCN_E_INVALID, std::string(who) + ": layer is NULL");
+  if (L->f_in <= 0 || L->f_out <= 0) return fail(GCN_E_INVALID, std::string(who) + ": non-positive width");
+  if (L->ld_in < L->f_in || L->ld_out < L->f_out)
+    return fail(GCN_E_INVALID, std::string(who) + ": pitch smaller than width");
+  if (L->act < GCN_ACT_NONE || L->act > GCN_ACT_SOFTMAX_CE)
+    return fail(GCN_E_INVALID, std::string(who) + ": unknown activation");
+  if (L->order < GCN_ORDER_AUTO || L->order > GCN_AGGREGATE_FIRST)
+    return fail(GCN_E_INVALID, std::string(who) + ": unknown order");
+  if (L->act == GCN_ACT_SOFTMAX_CE && L->f_out > 256)
+    return fail(GCN_E_UNSUPPORTED, std::string(who) + ": softmax cross-entropy needs f_out <= 256");
+  return GCN_OK;
+}
+
+gcn_status check_sparse(const gcn_sparse_x* x, const gcn_graph* g, const gcn_layer* L, bool need_csc,
+                        const char* who) {
+  if (x->n != g->n || x->f != L->f_in)
+    return fail(GCN_E_INVALID, std::string(who) + ": sparse X shape does not match graph / layer");
+  if (!x->row_ptr || !x->col || !x->val) return fail(GCN_E_INVALID, std::string(who) + ": X_csr missing");
+  if (need_csc && (!x->col_ptr || !x->row || !x->cval))
+    return fail(GCN_E_INVALID, std::string(who) + ": X_csc missing");
+  return GCN_OK;
+}
+
+int64_t pitch4(int64_t w) { return round_up(w, 4); }
+
+int32_t resolve_order(const gcn_layer* L, bool x_sparse) {
+  if (L->order != GCN_ORDER_AUTO) return L->order;
+  if (L->act == GCN_ACT_SOFTMAX_CE || x_sparse) return GCN_TRANSFORM_FIRST;
+  // aggregate-first aggregates f_in columns forward (and again backward above
+  // layer 0); transform-first aggregates f_out columns in both passes
+  const int64_t af = (int64_t)L->f_in * (L->index > 0 ? 2 : 1);
+  return af < 2 * (int64_t)L->f_out ? GCN_AGGREGATE_FIRST : GCN_TRANSFORM_FIRST;
+}
+
+AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, float* Z, int64_t ldz) {
+  AggParams p{};
+  p.n = g->n;
+  p.row_ptr = g->row_ptr;
+  p.col = g->col_idx;
+  p.dinv = g->dinv;
+  p.M = M;
+  p.ldm = ldm;
+  p.w = w;
+  p.Z = Z;
+  p.ldz = ldz;
+  p.epi = AGG_NONE;
+  return p;
+}
+
+GemmParams gemm(int64_t m, int64_t n, int64_t k, const float* A, int64_t lda, bool ta, const float* B,
+                int64_t ldb, bool tb, float* C, int64_t ldc) {
+  GemmParams p{};
+  p.m = m;
+  p.n = n;
+  p.k = k;
+  p.A = A;
+  p.lda = lda;
+  p.ta = ta;
+  p.B = B;
+  p.ldb = ldb;
+  p.tb = tb;
+  p.C = C;
+  p.ldc = ldc;
+  p.epi = GEMM_NONE;
+  return p;
+}
+
+// ---------------------------------------------------------------------------
+// layer plans: the same function sizes the workspace (base == NULL) and runs
+// ---------------------------------------------------------------------------
+
+gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, const gcn_sparse_x* x,
+                     const float* W, const float* b, float* Hout, float* saved, const int32_t* labels,
+                     float* loss, float* logits, Arena& a, hipStream_t s) {
+  const int32_t n = g->n;
+  const int32_t order = resolve_order(L, x != nullptr);
+  const bool run = a.base != nullptr;
+  if (order == GCN_AGGREGATE_FIRST) {
+    // P = A_hat H_in (kept for the backward pass), then H_out = act(P W + b)
+    if (run) {
+      AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in);
+      GCN_TRY(launch_aggregate(p, g->nnz, s));
+      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
+      q.bias = b;
+      q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
+      GCN_TRY(launch_gemm(q, nullptr, s));
+    }
+    return GCN_OK;
+  }
+  // transform-first: M = H_in W (or X_csr W), then Z = A_hat M + b with the epilogue
+  const int64_t ldm = pitch4(L->f_out);
+  float* M = a.take<float>((int64_t)n * ldm);
+  float* row_loss = L->act == GCN_ACT_SOFTMAX_CE ? a.take<float>(n) : nullptr;
+  void* cws = L->act == GCN_ACT_SOFTMAX_CE ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+  if (!run) return GCN_OK;
+  if (x) {
+    AggParams p{};
+    p.n = n;
+    p.row_ptr = x->row_ptr;
+    p.col = x->col;
+    p.val = x->val;
+    p.M = W;
+    p.ldm = L->f_out;
+    p.w = L->f_out;
+    p.Z = M;
+    p.ldz = ldm;
+    p.epi = AGG_NONE;
+    GCN_TRY(launch_aggregate(p, x->nnz, s));
+  } else {
+    GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
+    GCN_TRY(launch_gemm(q, nullptr, s));
+  }
+  AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out);
+  p.bias = b;
+  if (L->act == GCN_ACT_RELU) p.epi = AGG_RELU;
+  if (L->act == GCN_ACT_SOFTMAX_CE) {
+    p.epi = AGG_SOFTMAX;
+    p.labels = labels;
+    p.row_loss = row_loss;
+    p.logits = logits;
+    p.ldl = L->ld_out;
+    p.inv_n = n > 0 ? 1.f / (float)n : 0.f;
+  }
+  GCN_TRY(launch_aggregate(p, g->nnz, s));
+  if (L->act == GCN_ACT_SOFTMAX_CE)
+    GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
+  return GCN_OK;
+}
+
+gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, const float* Hin,
+                     const gcn_sparse_x* x, const float* saved, const float* W, float* dW, float* db,
+                     float* Gprev, Arena& a, hipStream_t s) {
+  const int32_t n = g->n;
+  const int32_t order = resolve_order(L, x != nullptr);
+  const bool run = a.base != nullptr;
+  void* cws = a.take<char>((int64_t)colsum_workspace(n, L->f_out));
+  if (order == GCN_AGGREGATE_FIRST) {
+    // Z = P W + b with P = A_hat H_in: dW = P^T G; dP = G W^T; G_prev = (A_hat dP) * 1[H_in > 0]
+    GemmParams dw = gemm(L->f_in, L->f_out, n, saved, L->ld_in, true, G, L->ld_out, false, dW, L->f_out);
+    void* gws = a.take<char>((int64_t)gemm_workspace(dw));
+    const int64_t ldt = pitch4(L->f_in);
+    float* T = Gprev ? a.take<float>((int64_t)n * ldt) : nullptr;
+    if (!run) return GCN_OK;
+    GCN_TRY(launch_gemm(dw, gws, s));
+    GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
+    if (Gprev) {
+      GemmParams t = gemm(n, L->f_in, L->f_out, G, L->ld_out, false, W, L->f_out, true, T, ldt);
+      GCN_TRY(launch_gemm(t, nullptr, s));
+      AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in);
+      p.epi = AGG_MASK;
+      p.mask = Hin;
+      p.ldmask = L->ld_in;
+      GCN_TRY(launch_aggregate(p, g->nnz, s));
+    }
+    return GCN_OK;
+  }
+  // transform-first: Q = A_hat G; dW = H_in^T Q (X_csc Q); G_prev = (Q W^T) * 1[H_in > 0]
+  const int64_t ldq = pitch4(L->f_out);
+  float* Q = a.take<float>((int64_t)n * ldq);
+  GemmParams dw = gemm(L->f_in, L->f_out, n, Hin, L->ld_in, true, Q, ldq, false, dW, L->f_out);
+  void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(dw));
+  if (!run) return GCN_OK;
+  GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq), g->nnz, s));
+  if (x) {
+    AggParams p{};
+    p.n = x->f;
+    p.row_ptr = x->col_ptr;
+    p.col = x->row;
+    p.val = x->cval;
+    p.M = Q;
+    p.ldm = ldq;
+    p.w = L->f_out;
+    p.Z = dW;
+    p.ldz = L->f_out;
+    p.epi = AGG_NONE;
+    GCN_TRY(launch_aggregate(p, x->nnz, s));
+  } else {
+    GCN_TRY(launch_gemm(dw, gws, s));
+  }
+  GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
+  if (Gprev) {
+    GemmParams t = gemm(n, L->f_in, L->f_out, Q, ldq, false, W, L->f_out, true, Gprev, L->ld_in);
+    t.epi = GEMM_MASK;
+    t.mask = Hin;
+    t.ldmask = L->ld_in;
+    GCN_TRY(launch_gemm(t, nullptr, s));
+  }
+  return GCN_OK;
+}
+
+gcn_status validate_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, const gcn_sparse_x* x,
+                        const float* W, float* Hout, float* saved, const int32_t* labels, float* loss,
+                        const char* who) {
+  GCN_TRY(check_graph(g, who));
+  GCN_TRY(check_layer(L, who));
+  if ((Hin == nullptr) == (x == nullptr))
+    return fail(GCN_E_INVALID, std::string(who) + ": exactly one of d_Hin and x must be given");
+  if (x) GCN_TRY(check_sparse(x, g, L, false, who));
+  if (!W || !Hout) return fail(GCN_E_INVALID, std::string(who) + ": d_W and d_Hout are required");
+  const int32_t order = resolve_order(L, x != nullptr);
+  if (order == GCN_AGGREGATE_FIRST) {
+    if (x) return fail(GCN_E_UNSUPPORTED, std::string(who) + ": aggregate-first needs dense input");
+    if (L->act == GCN_ACT_SOFTMAX_CE)
+      return fail(GCN_E_UNSUPPORTED, std::string(who) + ": aggregate-first with softmax cross-entropy");
+    if (!saved) return fail(GCN_E_INVALID, std::string(who) + ": aggregate-first needs d_saved");
+  }
+  if (L->act == GCN_ACT_SOFTMAX_CE && (!labels || !loss))
+    return fail(GCN_E_INVALID, std::string(who) + ": softmax cross-entropy needs labels and d_loss");
+  return GCN_OK;
+}
+
+gcn_status validate_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, const float* Hin,
+                        const gcn_sparse_x* x, const float* saved, const float* W, float* dW, float* db,
+                        float* Gprev, const char* who) {
+  GCN_TRY(check_graph(g, who));
+  GCN_TRY(check_layer(L, who));
+  if (!G || !W || !dW || !db) return fail(GCN_E_INVALID, std::string(who) + ": G, W, dW and db are required");
+  if (x) {
+    GCN_TRY(check_sparse(x, g, L, true, who));
+    if (Gprev) return fail(GCN_E_INVALID, std::string(who) + ": no input gradient for sparse X");
+  } else if (!Hin) {
+    return fail(GCN_E_INVALID, std::string(who) + ": d_Hin is required for a dense input");
+  }
+  const int32_t order = resolve_order(L, x != nullptr);
+  if (order == GCN_AGGREGATE_FIRST && !saved)
+    return fail(GCN_E_INVALID, std::string(who) + ": aggregate-first needs d_saved");
+  if (order == GCN_AGGREGATE_FIRST && x)
+    return fail(GCN_E_UNSUPPORTED, std::string(who) + ": aggregate-first needs dense input");
+  return GCN_OK;
+}
+
+}  // namespace
+}  // namespace gcn
+
+using namespace gcn;
+
+extern "C" {
+
+const char* gcn_status_string(gcn_status s) {
+  switch (s) {
+    case GCN_OK: return "GCN_OK";
+    case GCN_E_INVALID: return "GCN_E_INVALID";
+    case GCN_E_RANGE: return "GCN_E_RANGE";
+    case GCN_E_OVERFLOW: return "GCN_E_OVERFLOW";
+    case GCN_E_CAPACITY: return "GCN_E_CAPACITY";
+    case GCN_E_HIP: return "GCN_E_HIP";
+    case GCN_E_UNSUPPORTED: return "GCN_E_UNSUPPORTED";
+    default: return "GCN_E_UNKNOWN";
+  }
+}
+
+const char* gcn_last_error(void) { return g_err.c_str(); }
+
+int32_t gcn_version(void) { return 1; }
+
+int32_t gcn_layer_order(const gcn_layer* L, int32_t x_sparse) {
+  return L ? resolve_order(L, x_sparse != 0) : GCN_TRANSFORM_FIRST;
+}
+
+gcn_status gcn_build_csr(int32_t n, int64_t n_edges, const int32_t* d_src, const int32_t* d_dst,
+                         gcn_graph* g, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (n < 0 || n_edges < 0) return fail(GCN_E_INVALID, "gcn_build_csr: negative size");
+  if (n_edges >= (int64_t(1) << 30))
+    return fail(GCN_E_OVERFLOW, "gcn_build_csr: more than 2^30 input pairs (row counts are int32)");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, build_csr_workspace(n, n_edges), "gcn_build_csr", &query));
+  if (query) return GCN_OK;
+  if (!g) return fail(GCN_E_INVALID, "gcn_build_csr: graph is NULL");
+  if (n_edges > 0 && (!d_src || !d_dst)) return fail(GCN_E_INVALID, "gcn_build_csr: edge arrays missing");
+  if (!g->row_ptr || (n > 0 && (!g->deg || !g->dinv || !g->col_idx)))
+    return fail(GCN_E_INVALID, "gcn_build_csr: output arrays missing");
+  if (g->nnz_cap < 0) return fail(GCN_E_INVALID, "gcn_build_csr: negative capacity");
+  g->n = n;
+  return run_build_csr(n, n_edges, d_src, d_dst, g, d_ws, stream);
+}
+
+gcn_status gcn_feature_stats(const float* d_X, int32_t n, int32_t f, int64_t ldx, int32_t tau_num,
+                             int32_t tau_den, int32_t force_mode, int64_t* d_row_nnz,
+                             gcn_feature_info* info, gcn_sparse_x* x, void* d_ws, size_t* ws_bytes,
+                             hipStream_t stream) {
+  g_err.clear();
+  if (n < 0 || f < 0 || ldx < f) return fail(GCN_E_INVALID, "gcn_feature_stats: bad shape or pitch");
+  if (tau_den <= 0 || tau_num < 0) return fail(GCN_E_INVALID, "gcn_feature_stats: tau must be >= 0 with tau_den > 0");
+  if (force_mode < -1 || force_mode > GCN_SPARSE) return fail(GCN_E_INVALID, "gcn_feature_stats: bad force_mode");
+  const bool csc = x && x->col_ptr;
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, feature_stats_workspace(n, f, csc), "gcn_feature_stats", &query));
+  if (query) return GCN_OK;
+  if (!info || (n > 0 && f > 0 && !d_X)) return fail(GCN_E_INVALID, "gcn_feature_stats: X and info are required");
+  if (x && (!x->row_ptr || !x->col || !x->val || (csc && (!x->row || !x->cval))))
+    return fail(GCN_E_INVALID, "gcn_feature_stats: sparse output arrays missing");
+  return run_feature_stats(d_X, n, f, ldx, tau_num, tau_den, force_mode, d_row_nnz, info, x, d_ws, stream);
+}
+
+gcn_status gcn_layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* d_Hin,
+                         const gcn_sparse_x* x, const float* d_W, const float* d_b, float* d_Hout,
+                         float* d_saved, const int32_t* d_labels, float* d_loss, float* d_logits,
+                         void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  GCN_TRY(validate_fwd(g, L, d_Hin, x, d_W, d_Hout, d_saved, d_labels, d_loss, "gcn_layer_fwd"));
+  Arena plan;
+  GCN_TRY(layer_fwd(g, L, d_Hin, x, d_W, d_b, d_Hout, d_saved, d_labels, d_loss, d_logits, plan, stream));
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, plan.used, "gcn_layer_fwd", &query));
+  if (query) return GCN_OK;
+  Arena a;
+  a.base = static_cast<char*>(d_ws);
+  return layer_fwd(g, L, d_Hin, x, d_W, d_b, d_Hout, d_saved, d_labels, d_loss, d_logits, a, stream);
+}
+
+gcn_status gcn_layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* d_G, const float* d_Hin,
+                         const gcn_sparse_x* x, const float* d_saved, const float* d_W, float* d_dW,
+                         float* d_db, float* d_Gprev, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  GCN_TRY(validate_bwd(g, L, d_G, d_Hin, x, d_saved, d_W, d_dW, d_db, d_Gprev, "gcn_layer_bwd"));
+  Arena plan;
+  GCN_TRY(layer_bwd(g, L, d_G, d_Hin, x, d_saved, d_W, d_dW, d_db, d_Gprev, plan, stream));
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, plan.used, "gcn_layer_bwd", &query));
+  if (query) return GCN_OK;
+  Arena a;
+  a.base = static_cast<char*>(d_ws);
+  return layer_bwd(g, L, d_G, d_Hin, x, d_saved, d_W, d_dW, d_db, d_Gprev, a, stream);
+}
+
+gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const gcn_sparse_x* x,
+                     const int32_t* d_labels, float* d_loss, void* d_ws, size_t* ws_bytes,
+                     hipStream_t stream) {
+  g_err.clear();
+  const char* who = "gcn_epoch";
+  if (!m || !m->layers || m->n_layers <= 0) return fail(GCN_E_INVALID, "gcn_epoch: model has no layers");
+  const int L = m->n_layers;
+  if (2 * L > 16) return fail(GCN_E_UNSUPPORTED, "gcn_epoch: at most 8 layers");
+  if (!m->W || !m->b || !m->dW || !m->db || !m->mW || !m->vW || !m->mb || !m->vb || !m->act || !m->grad)
+    return fail(GCN_E_INVALID, "gcn_epoch: model pointer arrays missing");
+  for (int l = 0; l < L; ++l) {
+    const gcn_layer* ly = &m->layers[l];
+    GCN_TRY(check_layer(ly, who));
+    if (ly->index != l) return fail(GCN_E_INVALID, "gcn_epoch: layers[l].index must be l");
+    if (l > 0 && (ly->f_in != m->layers[l - 1].f_out || ly->ld_in != m->layers[l - 1].ld_out))
+      return fail(GCN_E_INVALID, "gcn_epoch: consecutive layer widths / pitches disagree");
+    if ((l == L - 1) != (ly->act == GCN_ACT_SOFTMAX_CE))
+      return fail(GCN_E_INVALID, "gcn_epoch: softmax cross-entropy must be the last layer's activation");
+    if (!m->W[l] || !m->dW[l] || !m->db[l] || !m->mW[l] || !m->vW[l] || !m->grad[l] || !m->b[l] ||
+        !m->mb[l] || !m->vb[l] || (l < L - 1 && !m->act[l]))
+      return fail(GCN_E_INVALID, "gcn_epoch: a layer buffer is NULL");
+  }
+  if (x && !x->col_ptr) return fail(GCN_E_INVALID, "gcn_epoch: the sparse path needs X_csc");
+  // validate every layer call, then plan the workspace as the maximum over the layer calls
+  size_t need = 0;
+  for (int l = 0; l < L; ++l) {
+    const gcn_layer* ly = &m->layers[l];
+    const float* Hin = l == 0 ? d_X : m->act[l - 1];
+    const gcn_sparse_x* xl = l == 0 ? x : nullptr;
+    float* Hout = l < L - 1 ? m->act[l] : m->grad[l];
+    float* saved = m->saved ? m->saved[l] : nullptr;
+    GCN_TRY(validate_fwd(g, ly, Hin, xl, m->W[l], Hout, saved, d_labels, d_loss, who));
+    GCN_TRY(validate_bwd(g, ly, m->grad[l], Hin, xl, saved, m->W[l], m->dW[l], m->db[l],
+                         l > 0 ? m->grad[l - 1] : nullptr, who));
+    Arena pf, pb;
+    GCN_TRY(layer_fwd(g, ly, Hin, xl, m->W[l], m->b[l], Hout, saved, d_labels, d_loss, nullptr, pf, stream));
+    GCN_TRY(layer_bwd(g, ly, m->grad[l], Hin, xl, saved, m->W[l], m->dW[l], m->db[l],
+                      l > 0 ? m->grad[l - 1] : nullptr, pb, stream));
+    need = std::max(need, std::max(pf.used, pb.used));
+  }
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, need, who, &query));
+  if (query) return GCN_OK;
+  for (int l = 0; l < L; ++l) {
+    Arena a;
+    a.base = static_cast<char*>(d_ws);
+    const gcn_layer* ly = &m->layers[l];
+    GCN_TRY(layer_fwd(g, ly, l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr, m->W[l], m->b[l],
+                      l < L - 1 ? m->act[l] : m->grad[l], m->saved ? m->saved[l] : nullptr, d_labels,
+                      d_loss, nullptr, a, stream));
+  }
+  for (int l = L - 1; l >= 0; --l) {
+    Arena a;
+    a.base = static_cast<char*>(d_ws);
+    const gcn_layer* ly = &m->layers[l];
+    GCN_TRY(layer_bwd(g, ly, m->grad[l], l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr,
+                      m->saved ? m->saved[l] : nullptr, m->W[l], m->dW[l], m->db[l],
+                      l > 0 ? m->grad[l - 1] : nullptr, a, stream));
+  }
+  gcn_adam_tensor t[16];
+  for (int l = 0; l < L; ++l) {
+    const int64_t fi = m->layers[l].f_in, fo = m->layers[l].f_out;
+    t[2 * l] = gcn_adam_tensor{m->W[l], m->dW[l], m->mW[l], m->vW[l], fi * fo};
+    t[2 * l + 1] = gcn_adam_tensor{m->b[l], m->db[l], m->mb[l], m->vb[l], fo};
+  }
+  GCN_TRY(launch_adam(t, 2 * L, m->step + 1, m->lr, m->beta1, m->beta2, m->eps, stream));
+  m->step += 1;
+  return GCN_OK;
+}
+
+gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm, const float* d_bias,
+                         int32_t epi, const float* d_mask, int64_t ldmask, float* d_Z, int64_t ldz,
+                         hipStream_t stream) {
+  g_err.clear();
+  GCN_TRY(check_graph(g, "gcn_aggregate"));
+  if (w < 0 || ldm < w || ldz < w) return fail(GCN_E_INVALID, "gcn_aggregate: bad width or pitch");
+  if (epi < GCN_EPI_NONE || epi > GCN_EPI_MASK) return fail(GCN_E_INVALID, "gcn_aggregate: unknown epilogue");
+  if (epi == GCN_EPI_MASK && (!d_mask || ldmask < w)) return fail(GCN_E_INVALID, "gcn_aggregate: mask missing");
+  if (g->n > 0 && w > 0 && (!d_M || !d_Z)) return fail(GCN_E_INVALID, "gcn_aggregate: d_M and d_Z are required");
+  AggParams p = graph_agg(g, w, d_M, ldm, d_Z, ldz);
+  p.bias = d_bias;
+  p.epi = epi == GCN_EPI_RELU ? AGG_RELU : (epi == GCN_EPI_MASK ? AGG_MASK : AGG_NONE);
+  p.mask = d_mask;
+  p.ldmask = ldmask;
+  return launch_aggregate(p, g->nnz, stream);
+}
+
+gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_A, int64_t lda,
+                    const float* d_B, int64_t ldb, float* d_C, int64_t ldc, const float* d_bias, int32_t epi,
+                    const float* d_mask, int64_t ldmask, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (op < GCN_OP_NN || op > GCN_OP_TN) return fail(GCN_E_INVALID, "gcn_gemm: unknown op");
+  if (m < 0 || n < 0 || k < 0) return fail(GCN_E_INVALID, "gcn_gemm: negative size");
+  const bool ta = op == GCN_OP_TN, tb = op == GCN_OP_NT;
+  if (lda < (ta ? m : k) || ldb < (tb ? k : n) || ldc < n) return fail(GCN_E_INVALID, "gcn_gemm: pitch too small");
+  if (epi < GCN_EPI_NONE || epi > GCN_EPI_MASK) return fail(GCN_E_INVALID, "gcn_gemm: unknown epilogue");
+  if (epi == GCN_EPI_MASK && (!d_mask || ldmask < n)) return fail(GCN_E_INVALID, "gcn_gemm: mask missing");
+  GemmParams p = gemm(m, n, k, d_A, lda, ta, d_B, ldb, tb, d_C, ldc);
+  p.bias = d_bias;
+  p.epi = epi == GCN_EPI_RELU ? GEMM_RELU : (epi == GCN_EPI_MASK ? GEMM_MASK : GEMM_NONE);
+  p.mask = d_mask;
+  p.ldmask = ldmask;
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, gemm_workspace(p), "gcn_gemm", &query));
+  if (query) return GCN_OK;
+  if (m > 0 && n > 0 && (!d_C || (k > 0 && (!d_A || !d_B)))) return fail(GCN_E_INVALID, "gcn_gemm: NULL operand");
+  if (gemm_workspace(p) > 0 && p.epi != GEMM_NONE)
+    return fail(GCN_E_UNSUPPORTED, "gcn_gemm: split-k launches support only the bias epilogue");
+  return launch_gemm(p, d_ws, stream);
+}
+
+gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, const float* d_val,
+                    int64_t b_rows, int32_t w, const float* d_B, int64_t ldb, float* d_C, int64_t ldc,
+                    hipStream_t stream) {
+  g_err.clear();
+  if (nrows < 0 || nrows > INT32_MAX || w < 0 || b_rows < 0 || ldb < w || ldc < w)
+    return fail(GCN_E_INVALID, "gcn_spmm: bad size or pitch");
+  if (nrows > 0 && w > 0 && (!d_ptr || !d_idx || !d_val || !d_B || !d_C))
+    return fail(GCN_E_INVALID, "gcn_spmm: NULL argument");
+  AggParams p{};
+  p.n = (int32_t)nrows;
+  p.row_ptr = d_ptr;
+  p.col = d_idx;
+  p.val = d_val;
+  p.M = d_B;
+  p.ldm = ldb;
+  p.w = w;
+  p.Z = d_C;
+  p.ldz = ldc;
+  p.epi = AGG_NONE;
+  return launch_aggregate(p, -1, stream);
+}
+
+gcn_status gcn_column_sums(int64_t rows, int32_t w, const float* d_G, int64_t ldg, float* d_out,
+                           const float* d_row_vals, float* d_mean, void* d_ws, size_t* ws_bytes,
+                           hipStream_t stream) {
+  g_err.clear();
+  if (rows < 0 || w < 0 || ldg < w) return fail(GCN_E_INVALID, "gcn_column_sums: bad size or pitch");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, colsum_workspace(rows, w), "gcn_column_sums", &query));
+  if (query) return GCN_OK;
+  if ((w > 0 && (!d_out || (rows > 0 && !d_G))) || (d_row_vals && !d_mean) || (rows > 0 && d_mean && !d_row_vals))
+    return fail(GCN_E_INVALID, "gcn_column_sums: NULL argument");
+  return launch_colsum(rows, w, d_G, ldg, d_out, d_row_vals, d_mean, d_ws, stream);
+}
+
+gcn_status gcn_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, double lr, double beta1,
+                    double beta2, double eps, hipStream_t stream) {
+  g_err.clear();
+  if (count < 0 || (count > 0 && !t) || step < 1) return fail(GCN_E_INVALID, "gcn_adam: bad arguments");
+  for (int i = 0; i < count; ++i)
+    if (t[i].count < 0 || (t[i].count > 0 && (!t[i].param || !t[i].grad || !t[i].m || !t[i].v)))
+      return fail(GCN_E_INVALID, "gcn_adam: bad tensor");
+  return launch_adam(t, count, step, lr, beta1, beta2, eps, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,356 @@
+// gemm.hip -- dense fp32 products on the gfx950 matrix cores.
+//
+// The dense-path transforms of Algorithm 1 (GEMM(X, W) forward, GEMM^T(X, G)
+// backward) plus the input-gradient product Q W^T of backpropagation:
+//   C(m, n) = sum_k A(m, k) B(k, n)
+// with either operand read transposed.  One workgroup computes a BM x BN tile
+// with WM x WN wavefronts, each issuing v_mfma_f32_32x32x2_f32 on 32 x 32
+// sub-tiles.  K is walked in BK-wide slabs staged through LDS with two
+// buffers: the next slab's global loads are in flight while the matrix cores
+// work on the current one.  Each operand is staged in the layout it has in
+// memory (no transposing stores): "k-contiguous" slabs are read back as
+// 16-byte vectors, "m/n-contiguous" slabs as one conflict-free dword per lane.
+// The k index inside a slab is permuted consistently for A and B (lane half h
+// takes k = h*BK/2 + kk), which a sum over k does not notice.
+//
+// Epilogues: + bias, ReLU, or multiplication by 1[mask > 0]; or, for a
+// split-k launch, a plain store of the partial tile into the workspace, summed
+// afterwards in a fixed order by k_splitk_reduce (deterministic, no atomics).
+#include "internal.h"
+
+namespace gcn {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kPad = 4;
+
+struct GemmArgs {
+  GemmParams p;
+  float* part;     // split-k partial tiles (split index major), or NULL
+  int64_t kchunk;  // k extent per split
+  int a_vec;       // A rows are 16-byte aligned with pitch % 4 == 0
+  int b_vec;
+};
+
+// Load 4 consecutive elements src[i .. i+3] (i < lim are valid) into v.
+__device__ __forceinline__ float4 load4(const float* src, int64_t i, int64_t lim, bool vec) {
+  if (vec && i + 4 <= lim) return *reinterpret_cast<const float4*>(src + i);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i + 0 < lim) v.x = src[i + 0];
+  if (i + 1 < lim) v.y = src[i + 1];
+  if (i + 2 < lim) v.z = src[i + 2];
+  if (i + 3 < lim) v.w = src[i + 3];
+  return v;
+}
+
+// Staging of one operand slab.  Operand X(r, k) with r in [r0, r0+R) (r < rlim)
+// and k in [k0, k0+BK) (k < klim).  KCONT: X(r,k) = src[r*ld + k], else
+// src[k*ld + r].  LDS layout: KCONT -> [R][BK+kPad], else [BK][R+kPad].
+template <int R, int BK, int NT, bool KCONT>
+struct Stage {
+  static constexpr int kChunks = R * BK / 4;
+  static constexpr int kPer = (kChunks + NT - 1) / NT;
+  static constexpr int kLdsFloats = KCONT ? R * (BK + kPad) : BK * (R + kPad);
+  float4 reg[kPer];
+
+  __device__ __forceinline__ void load(const float* src, int64_t ld, int64_t r0, int64_t rlim,
+                                       int64_t k0, int64_t klim, bool vec, int tid) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = tid + i * NT;
+      reg[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c < kChunks) {
+        if (KCONT) {
+          const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
+          if (r0 + r < rlim) reg[i] = load4(src + (r0 + r) * ld, k0 + kq, klim, vec);
+        } else {
+          const int kr = c / (R / 4), rq = (c % (R / 4)) * 4;
+          if (k0 + kr < klim) reg[i] = load4(src + (k0 + kr) * ld, r0 + rq, rlim, vec);
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = tid + i * NT;
+      if (c < kChunks) {
+        if (KCONT) {
+          const int r = c / (BK / 4), kq = (c % (BK / 4)) * 4;
+          *reinterpret_cast<float4*>(lds + r * (BK + kPad) + kq) = reg[i];
+        } else {
+          const int kr = c / (R / 4), rq = (c % (R / 4)) * 4;
+          *reinterpret_cast<float4*>(lds + kr * (R + kPad) + rq) = reg[i];
+        }
+      }
+    }
+  }
+  // fragment value for sub-tile row rr (0..R-1), slab k index kidx
+  static __device__ __forceinline__ float frag(const float* lds, int rr, int kidx) {
+    return KCONT ? lds[rr * (BK + kPad) + kidx] : lds[kidx * (R + kPad) + rr];
+  }
+};
+
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
+  constexpr int NT = WM * WN * 64;
+  constexpr int TM = BM / WM / 32;
+  constexpr int TN = BN / WN / 32;
+  constexpr int KH = BK / 2;
+  using SA = Stage<BM, BK, NT, !TA>;  // A(m,k): k-contiguous unless transposed
+  using SB = Stage<BN, BK, NT, TB>;   // B(k,n): n-contiguous unless transposed
+  __shared__ __attribute__((aligned(16))) float lds_a[2][SA::kLdsFloats];
+  __shared__ __attribute__((aligned(16))) float lds_b[2][SB::kLdsFloats];
+
+  const GemmParams& p = g.p;
+  const int tid = threadIdx.x;
+  const int wave = tid / 64, l = tid % 64;
+  const int wm = wave % WM, wn = wave / WM;
+  const int h = l / 32, l32 = l % 32;
+  const int64_t m0 = (int64_t)blockIdx.x * BM;
+  const int64_t n0 = (int64_t)blockIdx.y * BN;
+  int64_t kbeg = 0, kend = p.k;
+  if (SPLIT) {
+    kbeg = (int64_t)blockIdx.z * g.kchunk;
+    kend = kbeg + g.kchunk < p.k ? kbeg + g.kchunk : p.k;
+  }
+
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  SA sa;
+  SB sb;
+  // A operand: rows m, cols k.  TA: stored k x m.
+  auto load_slab = [&](int64_t k0) {
+    sa.load(p.A, p.lda, m0, p.m, k0, kend, g.a_vec, tid);
+    sb.load(p.B, p.ldb, n0, p.n, k0, kend, g.b_vec, tid);
+  };
+
+  const int64_t nslab = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (nslab > 0) {
+    load_slab(kbeg);
+    sa.store(lds_a[0], tid);
+    sb.store(lds_b[0], tid);
+  }
+  __syncthreads();
+  for (int64_t s = 0; s < nslab; ++s) {
+    const int buf = (int)(s & 1);
+    if (s + 1 < nslab) load_slab(kbeg + (s + 1) * BK);
+    const float* la = lds_a[buf];
+    const float* lb = lds_b[buf];
+    float af[TM][KH], bf[TN][KH];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int kk = 0; kk < KH; ++kk) af[i][kk] = SA::frag(la, wm * (BM / WM) + i * 32 + l32, h * KH + kk);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int kk = 0; kk < KH; ++kk) bf[j][kk] = SB::frag(lb, wn * (BN / WN) + j * 32 + l32, h * KH + kk);
+#pragma unroll
+    for (int kk = 0; kk < KH; ++kk)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
+    if (s + 1 < nslab) {
+      sa.store(lds_a[buf ^ 1], tid);
+      sb.store(lds_b[buf ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: lane l32 holds column l32 of each 32x32 sub-tile; register r holds
+  // row 8*(r/4) + 4*h + r%4.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int64_t col = n0 + wn * (BN / WN) + j * 32 + l32;
+      if (col >= p.n) continue;
+      const float bv = (!SPLIT && p.bias) ? p.bias[col] : 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * (BM / WM) + i * 32 + 8 * (r / 4) + 4 * h + (r % 4);
+        if (row >= p.m) continue;
+        float v = acc[i][j][r];
+        if (SPLIT) {
+          g.part[((int64_t)blockIdx.z * p.m + row) * p.n + col] = v;
+        } else {
+          v += bv;
+          if (EPI == GEMM_RELU) v = fmaxf(v, 0.f);
+          if (EPI == GEMM_MASK) v = p.mask[row * p.ldmask + col] > 0.f ? v : 0.f;
+          p.C[row * p.ldc + col] = v;
+        }
+      }
+    }
+  }
+}
+
+// C(m,n) = sum_s part[s](m,n) (+ bias) in split order.
+__global__ void __launch_bounds__(256) k_splitk_reduce(const float* part, int64_t splits, int64_t m,
+                                                       int64_t n, float* C, int64_t ldc,
+                                                       const float* bias) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= m * n) return;
+  const int64_t row = i / n, col = i % n;
+  float s = 0.f;
+  for (int64_t z = 0; z < splits; ++z) s += part[z * m * n + i];
+  if (bias) s += bias[col];
+  C[row * ldc + col] = s;
+}
+
+struct Shape {
+  int bm, bn;
+};
+
+Shape pick_shape(const GemmParams& p) {
+  if (p.n <= 32) return {256, 32};
+  if (p.n <= 64) return {256, 64};
+  return {128, 128};
+}
+
+int64_t pick_splits(const GemmParams& p, Shape sh) {
+  if (!p.ta) return 1;  // only A^T B reduces over the long (row) dimension
+  const int64_t tiles = ceil_div(p.m, sh.bm) * ceil_div(p.n, sh.bn);
+  int64_t s = ceil_div(2048, tiles);
+  const int64_t max_s = ceil_div(p.k, 256);
+  if (s > max_s) s = max_s;
+  return s < 1 ? 1 : s;
+}
+
+template <int BM, int BN, int WM, int WN, bool TA, bool TB>
+gcn_status launch_tile(const GemmArgs& g, int64_t splits, hipStream_t s) {
+  constexpr int BK = 16;
+  dim3 grid((unsigned)ceil_div(g.p.m, BM), (unsigned)ceil_div(g.p.n, BN), (unsigned)splits);
+  dim3 block(WM * WN * 64);
+  if (splits > 1) {
+    hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, true>), grid, block, 0, s, g);
+  } else {
+    switch (g.p.epi) {
+      case GEMM_RELU:
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_RELU, false>), grid, block, 0, s, g);
+        break;
+      case GEMM_MASK:
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_MASK, false>), grid, block, 0, s, g);
+        break;
+      default:
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, false>), grid, block, 0, s, g);
+    }
+  }
+  return check_launch("gemm");
+}
+
+template <bool TA, bool TB>
+gcn_status launch_layout(const GemmArgs& g, Shape sh, int64_t splits, hipStream_t s) {
+  if (sh.bn == 32) return launch_tile<256, 32, 4, 1, TA, TB>(g, splits, s);
+  if (sh.bn == 64) return launch_tile<256, 64, 4, 1, TA, TB>(g, splits, s);
+  return launch_tile<128, 128, 2, 2, TA, TB>(g, splits, s);
+}
+
+}  // namespace
+
+size_t gemm_workspace(const GemmParams& p) {
+  const Shape sh = pick_shape(p);
+  const int64_t s = pick_splits(p, sh);
+  return s > 1 ? sizeof(float) * (size_t)(s * p.m * p.n) : 0;
+}
+
+gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
+  if (p.m == 0 || p.n == 0) return GCN_OK;
+  const Shape sh = pick_shape(p);
+  const int64_t splits = p.k == 0 ? 1 : pick_splits(p, sh);
+  GemmArgs g;
+  g.p = p;
+  g.part = splits > 1 ? static_cast<float*>(ws) : nullptr;
+  g.kchunk = round_up(ceil_div(p.k, splits), 16);
+  g.a_vec = p.lda % 4 == 0 && aligned16(p.A);
+  g.b_vec = p.ldb % 4 == 0 && aligned16(p.B);
+  char name[64];
+  snprintf(name, sizeof name, "gemm_%s%s_%ldx%ldx%ld", p.ta ? "T" : "N", p.tb ? "T" : "N",
+           (long)p.m, (long)p.n, (long)p.k);
+  ProfScope prof(name, (int32_t)p.n, p.m, p.k, s);
+  gcn_status st;
+  if (!p.ta && !p.tb) st = launch_layout<false, false>(g, sh, splits, s);
+  else if (!p.ta && p.tb) st = launch_layout<false, true>(g, sh, splits, s);
+  else if (p.ta && !p.tb) st = launch_layout<true, false>(g, sh, splits, s);
+  else st = launch_layout<true, true>(g, sh, splits, s);
+  if (st != GCN_OK || splits == 1) return st;
+  const int64_t total = p.m * p.n;
+  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, s, g.part,
+                     splits, p.m, p.n, p.C, p.ldc, p.bias);
+  return check_launch("gemm split-k reduce");
+}
+
+// ---------------------------------------------------------------------------
+// column sums (bias gradient) and mean of per-row values (loss), fixed order
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kColBlocks = 512;
+constexpr int kColThreads = 256;
+
+// Block b sums rows [b*chunk, (b+1)*chunk): thread (c, r4) takes columns c, c+64, ...
+// and rows r4, r4+4, ...; the 4 row lanes are combined in LDS in index order.
+__global__ void __launch_bounds__(kColThreads) k_colsum_partial(int64_t rows, int32_t w,
+                                                                const float* G, int64_t ldg,
+                                                                int64_t chunk, const float* rv,
+                                                                double* part, int32_t pw) {
+  __shared__ double red[4][64];
+  const int c = threadIdx.x % 64, r4 = threadIdx.x / 64;
+  const int64_t r0 = (int64_t)blockIdx.x * chunk;
+  const int64_t r1 = r0 + chunk < rows ? r0 + chunk : rows;
+  for (int cb = 0; cb < pw; cb += 64) {
+    const int col = cb + c;
+    double s = 0.0;
+    if (col < w) {
+      for (int64_t r = r0 + r4; r < r1; r += 4) s += (double)G[r * ldg + col];
+    } else if (col == w && rv) {
+      for (int64_t r = r0 + r4; r < r1; r += 4) s += (double)rv[r];
+    }
+    red[r4][c] = s;
+    __syncthreads();
+    if (r4 == 0 && col < pw) part[(int64_t)blockIdx.x * pw + col] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(256) k_colsum_final(const double* part, int nblk, int32_t w,
+                                                      int32_t pw, float* out, float* mean,
+                                                      double inv_rows) {
+  for (int col = threadIdx.x; col < pw; col += 256) {
+    double s = 0.0;
+    for (int b = 0; b < nblk; ++b) s += part[(int64_t)b * pw + col];
+    if (col < w) out[col] = (float)s;
+    else if (mean && col == w) *mean = (float)(s * inv_rows);
+  }
+}
+}  // namespace
+
+size_t colsum_workspace(int64_t rows, int32_t w) {
+  (void)rows;
+  return sizeof(double) * (size_t)kColBlocks * (size_t)(w + 1);
+}
+
+gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, float* out,
+                         const float* row_vals, float* mean, void* ws, hipStream_t s) {
+  const int32_t pw = w + (row_vals ? 1 : 0);
+  if (pw == 0) return GCN_OK;
+  const int64_t chunk = rows > 0 ? ceil_div(rows, kColBlocks) : 1;
+  const int nblk = kColBlocks;
+  double* part = static_cast<double*>(ws);
+  hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(kColThreads), 0, s, rows, w, G, ldg, chunk,
+                     row_vals, part, pw);
+  GCN_TRY(check_launch("column sums"));
+  hipLaunchKernelGGL(k_colsum_final, dim3(1), dim3(256), 0, s, part, nblk, w, pw, out, mean,
+                     rows > 0 ? 1.0 / (double)rows : 0.0);
+  return check_launch("column sums final");
+}
+
+}  // namespace gcn

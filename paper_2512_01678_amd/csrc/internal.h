@@ -1,0 +1,136 @@
+// internal.h -- declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstddef>
+#include <cstdio>
+#include <cstdint>
+#include <string>
+
+#include "gcn.h"
+
+namespace gcn {
+
+// ---------------------------------------------------------------------------
+// errors
+// ---------------------------------------------------------------------------
+gcn_status fail(gcn_status s, const std::string& msg);
+gcn_status hip_fail(hipError_t e, const char* what);
+inline gcn_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? GCN_OK : hip_fail(e, what);
+}
+
+#define GCN_TRY(expr)                      \
+  do {                                     \
+    gcn_status _s = (expr);                \
+    if (_s != GCN_OK) return _s;           \
+  } while (0)
+
+#define GCN_HIP(expr, what)                          \
+  do {                                               \
+    hipError_t _e = (expr);                          \
+    if (_e != hipSuccess) return hip_fail(_e, what); \
+  } while (0)
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Sub-allocator over a caller workspace: first pass measures, second pass carves.
+struct Arena {
+  char* base = nullptr;  // NULL while measuring
+  size_t used = 0;
+  template <class T>
+  T* take(int64_t count) {
+    used = (size_t)round_up((int64_t)used, 256);
+    T* p = base ? reinterpret_cast<T*>(base + used) : nullptr;
+    used += sizeof(T) * (size_t)(count > 0 ? count : 0);
+    return p;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// profiling hooks (events around launches; no-ops when disabled)
+// ---------------------------------------------------------------------------
+struct ProfScope {
+  int slot = -1;
+  hipStream_t stream = nullptr;
+  ProfScope(const char* name, int32_t width, int64_t rows, int64_t nnz, hipStream_t s);
+  ~ProfScope();
+};
+
+// ---------------------------------------------------------------------------
+// launchers (each validates nothing: callers in api.hip validate first)
+// ---------------------------------------------------------------------------
+enum AggEpi { AGG_NONE = 0, AGG_RELU = 1, AGG_MASK = 2, AGG_SOFTMAX = 3 };
+
+struct AggParams {
+  int32_t n;               // output rows
+  const int64_t* row_ptr;  // n + 1
+  const int32_t* col;      // neighbours / column indices
+  const float* dinv;       // normalised aggregation: dinv weights (else NULL)
+  const float* val;        // stored values (sparse products), else NULL
+  const float* M;          // gathered rows
+  int64_t ldm;
+  int32_t w;
+  const float* bias;       // w or NULL
+  int32_t epi;             // AggEpi
+  const float* mask;       // AGG_MASK
+  int64_t ldmask;
+  float* Z;
+  int64_t ldz;
+  // softmax cross-entropy epilogue
+  const int32_t* labels;
+  float* row_loss;         // n: per-row loss
+  float* logits;           // optional copy of Z
+  int64_t ldl;
+  float inv_n;             // 1 / n
+};
+gcn_status launch_aggregate(const AggParams& p, int64_t nnz, hipStream_t s);
+
+enum GemmEpi { GEMM_NONE = 0, GEMM_RELU = 1, GEMM_MASK = 2 };
+// C(m,n) = sum_k A(m,k) B(k,n) with A(m,k) = A[m*lda+k] (ta=false) or A[k*lda+m] (ta=true),
+// B(k,n) = B[k*ldb+n] (tb=false) or B[n*ldb+k] (tb=true).
+struct GemmParams {
+  int64_t m, n, k;
+  const float* A;
+  int64_t lda;
+  bool ta;
+  const float* B;
+  int64_t ldb;
+  bool tb;
+  float* C;
+  int64_t ldc;
+  const float* bias;
+  int32_t epi;
+  const float* mask;
+  int64_t ldmask;
+};
+size_t gemm_workspace(const GemmParams& p);
+gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s);
+
+size_t colsum_workspace(int64_t rows, int32_t w);
+gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, float* out,
+                         const float* row_vals, float* mean, void* ws, hipStream_t s);
+
+// exclusive scan of int32 counts into int64 offsets out[0..n], out[n] = total
+size_t scan_workspace(int64_t n);
+gcn_status launch_scan_i32(const int32_t* in, int64_t n, int64_t* out, void* ws, hipStream_t s);
+
+size_t build_csr_workspace(int32_t n, int64_t n_edges);
+gcn_status run_build_csr(int32_t n, int64_t n_edges, const int32_t* src, const int32_t* dst,
+                         gcn_graph* g, void* ws, hipStream_t s);
+
+size_t feature_stats_workspace(int32_t n, int32_t f, bool want_csc);
+gcn_status run_feature_stats(const float* X, int32_t n, int32_t f, int64_t ldx, int32_t tau_num,
+                             int32_t tau_den, int32_t force_mode, int64_t* row_nnz,
+                             gcn_feature_info* info, gcn_sparse_x* x, void* ws, hipStream_t s);
+
+gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, double lr, double b1,
+                       double b2, double eps, hipStream_t s);
+
+}  // namespace gcn

@@ -1,0 +1,411 @@
+"""ctypes binding of libgcn.so (include/gcn.h).
+
+Argument marshalling only: every computation runs in the HIP library.  torch
+supplies device memory (tensor.data_ptr()) and the HIP stream
+(torch.cuda.current_stream().cuda_stream); nothing here computes on tensors.
+If libgcn.so is missing, importing this module raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgcn.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
+
+_lib = C.CDLL(LIB_PATH)
+
+P = C.c_void_p
+i32, i64, f32, f64, sz = C.c_int32, C.c_int64, C.c_float, C.c_double, C.c_size_t
+
+OK, E_INVALID, E_RANGE, E_OVERFLOW, E_CAPACITY, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+DENSE, SPARSE = 0, 1
+ACT_NONE, ACT_RELU, ACT_SOFTMAX_CE = 0, 1, 2
+ORDER_AUTO, TRANSFORM_FIRST, AGGREGATE_FIRST = 0, 1, 2
+EPI_NONE, EPI_RELU, EPI_MASK = 0, 1, 2
+OP_NN, OP_NT, OP_TN = 0, 1, 2
+
+
+class GcnError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        name = _lib.gcn_status_string(status).decode()
+        msg = _lib.gcn_last_error().decode()
+        super().__init__(f"{where}: {name}: {msg}")
+
+
+class gcn_graph(C.Structure):
+    _fields_ = [("n", i32), ("nnz", i64), ("nnz_cap", i64), ("row_ptr", P), ("col_idx", P),
+                ("deg", P), ("dinv", P)]
+
+
+class gcn_sparse_x(C.Structure):
+    _fields_ = [("n", i32), ("f", i32), ("nnz", i64), ("row_ptr", P), ("col", P), ("val", P),
+                ("col_ptr", P), ("row", P), ("cval", P)]
+
+
+class gcn_feature_info(C.Structure):
+    _fields_ = [("nnz", i64), ("sparsity", f64), ("mode", i32)]
+
+
+class gcn_layer(C.Structure):
+    _fields_ = [("f_in", i32), ("f_out", i32), ("ld_in", i64), ("ld_out", i64), ("act", i32),
+                ("order", i32), ("index", i32)]
+
+
+class gcn_model(C.Structure):
+    _fields_ = [("n_layers", i32), ("layers", C.POINTER(gcn_layer))] + \
+               [(nm, C.POINTER(P)) for nm in ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act",
+                                               "saved", "grad")] + \
+               [("lr", f64), ("beta1", f64), ("beta2", f64), ("eps", f64), ("step", i32)]
+
+
+class gcn_adam_tensor(C.Structure):
+    _fields_ = [("param", P), ("grad", P), ("m", P), ("v", P), ("count", i64)]
+
+
+class gcn_profile_record(C.Structure):
+    _fields_ = [("name", C.c_char * 64), ("width", i32), ("rows", i64), ("nnz", i64), ("ms", f32)]
+
+
+_SIG = {
+    "gcn_status_string": (C.c_char_p, [i32]),
+    "gcn_last_error": (C.c_char_p, []),
+    "gcn_version": (i32, []),
+    "gcn_build_csr": (i32, [i32, i64, P, P, C.POINTER(gcn_graph), P, C.POINTER(sz), P]),
+    "gcn_feature_stats": (i32, [P, i32, i32, i64, i32, i32, i32, P, C.POINTER(gcn_feature_info),
+                                C.POINTER(gcn_sparse_x), P, C.POINTER(sz), P]),
+    "gcn_layer_order": (i32, [C.POINTER(gcn_layer), i32]),
+    "gcn_layer_fwd": (i32, [C.POINTER(gcn_graph), C.POINTER(gcn_layer), P, C.POINTER(gcn_sparse_x),
+                            P, P, P, P, P, P, P, P, C.POINTER(sz), P]),
+    "gcn_layer_bwd": (i32, [C.POINTER(gcn_graph), C.POINTER(gcn_layer), P, P, C.POINTER(gcn_sparse_x),
+                            P, P, P, P, P, P, C.POINTER(sz), P]),
+    "gcn_epoch": (i32, [C.POINTER(gcn_model), C.POINTER(gcn_graph), P, C.POINTER(gcn_sparse_x), P, P,
+                        P, C.POINTER(sz), P]),
+    "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i32, P, i64, P, i64, P]),
+    "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
+    "gcn_spmm": (i32, [i64, P, P, P, i64, i32, P, i64, P, i64, P]),
+    "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
+    "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
+    "gcn_profile_enable": (i32, [i32]),
+    "gcn_profile_count": (i32, []),
+    "gcn_profile_read": (i32, [i32, C.POINTER(gcn_profile_record)]),
+    "gcn_profile_reset": (i32, []),
+}
+for _name, (_res, _args) in _SIG.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+def _check(status, where):
+    if status != OK:
+        raise GcnError(status, where)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def pitch(w: int) -> int:
+    """Row pitch used for library-owned activations: width rounded up to 4 floats."""
+    return (w + 3) // 4 * 4
+
+
+def padded(rows: int, w: int, device="cuda", fill=None):
+    """A rows x w fp32 view with pitch(w) columns of storage (extra columns zero)."""
+    buf = torch.zeros((rows, pitch(w)), dtype=torch.float32, device=device)
+    return buf[:, :w]
+
+
+def _ld(t):
+    return t.stride(0) if t.dim() == 2 else t.shape[-1]
+
+
+class _Workspace:
+    def __init__(self):
+        self.buf = None
+
+    def get(self, nbytes, device):
+        if nbytes == 0:
+            return None
+        if self.buf is None or self.buf.numel() < nbytes or self.buf.device != torch.device(device):
+            self.buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        return self.buf
+
+
+def _run_ws(fn, args_before, args_after, where, ws: _Workspace | None, device):
+    """Two-phase workspace protocol: size query, then the call with a buffer that large."""
+    nbytes = sz(0)
+    _check(fn(*args_before, None, C.byref(nbytes), *args_after), where + " (size query)")
+    ws = ws or _Workspace()
+    buf = ws.get(max(nbytes.value, 256), device)
+    nbytes = sz(buf.numel())
+    _check(fn(*args_before, buf.data_ptr(), C.byref(nbytes), *args_after), where)
+    return ws
+
+
+# ---------------------------------------------------------------------------
+# graph and features
+# ---------------------------------------------------------------------------
+
+
+class DeviceGraph:
+    """A + I in CSR on the device (owning torch tensors)."""
+
+    def __init__(self, n, row_ptr, col_idx, deg, dinv, nnz):
+        self.n = n
+        self.row_ptr, self.col_idx, self.deg, self.dinv = row_ptr, col_idx, deg, dinv
+        self.nnz = nnz
+        self.c = gcn_graph(n, nnz, col_idx.numel(), _ptr(row_ptr), _ptr(col_idx), _ptr(deg), _ptr(dinv))
+
+
+def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None) -> DeviceGraph:
+    """gcn_build_csr on device int32 edge arrays; returns the graph (blocking)."""
+    dev = src.device
+    ne = src.numel()
+    row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    col = torch.empty(max(2 * ne + n, 1), dtype=torch.int32, device=dev)
+    deg = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    dinv = torch.empty(max(n, 1), dtype=torch.float32, device=dev)
+    g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv))
+    _run_ws(_lib.gcn_build_csr, (n, ne, _ptr(src), _ptr(dst), C.byref(g)), (P(_stream(stream)),),
+            "gcn_build_csr", None, dev)
+    return DeviceGraph(n, row_ptr, col, deg, dinv, g.nnz)
+
+
+class SparseFeatures:
+    """X_csr (+ X_csc) on the device (owning torch tensors)."""
+
+    def __init__(self, n, f, nnz, dev, csc=True):
+        cap = max(nnz, 1)
+        self.row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
+        self.col = torch.empty(cap, dtype=torch.int32, device=dev)
+        self.val = torch.empty(cap, dtype=torch.float32, device=dev)
+        self.col_ptr = torch.empty(f + 1, dtype=torch.int64, device=dev) if csc else None
+        self.row = torch.empty(cap, dtype=torch.int32, device=dev) if csc else None
+        self.cval = torch.empty(cap, dtype=torch.float32, device=dev) if csc else None
+        self.c = gcn_sparse_x(n, f, nnz, _ptr(self.row_ptr), _ptr(self.col), _ptr(self.val),
+                              _ptr(self.col_ptr), _ptr(self.row), _ptr(self.cval))
+
+    @property
+    def nnz(self):
+        return self.c.nnz
+
+
+def feature_stats(X: torch.Tensor, tau=(4, 5), force_mode=-1, materialize=None, csc=True,
+                  row_nnz: torch.Tensor | None = None, stream=None):
+    """Density probe (+ X_csr / X_csc when materialize is True, or None -> by mode).
+
+    Returns (info dict, SparseFeatures or None).  Blocking.
+    """
+    n, f = X.shape
+    ld = _ld(X)
+    info = gcn_feature_info()
+    st = P(_stream(stream))
+    _run_ws(_lib.gcn_feature_stats, (_ptr(X), n, f, ld, tau[0], tau[1], force_mode, _ptr(row_nnz),
+                                     C.byref(info), None), (st,), "gcn_feature_stats", None, X.device)
+    out = dict(nnz=info.nnz, sparsity=info.sparsity, mode=info.mode)
+    want = (info.mode == SPARSE) if materialize is None else materialize
+    if not want:
+        return out, None
+    sx = SparseFeatures(n, f, info.nnz, X.device, csc=csc)
+    _run_ws(_lib.gcn_feature_stats, (_ptr(X), n, f, ld, tau[0], tau[1], force_mode, None,
+                                     C.byref(info), C.byref(sx.c)), (st,), "gcn_feature_stats",
+            None, X.device)
+    return out, sx
+
+
+# ---------------------------------------------------------------------------
+# lower-level steps
+# ---------------------------------------------------------------------------
+
+
+def aggregate(g: DeviceGraph, M: torch.Tensor, out: torch.Tensor, bias=None, epi=EPI_NONE, mask=None,
+              stream=None):
+    w = M.shape[1]
+    _check(_lib.gcn_aggregate(C.byref(g.c), w, _ptr(M), _ld(M), _ptr(bias), epi, _ptr(mask),
+                              _ld(mask) if mask is not None else 0, _ptr(out), _ld(out),
+                              P(_stream(stream))), "gcn_aggregate")
+    return out
+
+
+def gemm(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, ws: _Workspace | None = None, stream=None):
+    if op == OP_NN:
+        m, k = A.shape
+        n = B.shape[1]
+    elif op == OP_NT:
+        m, k = A.shape
+        n = B.shape[0]
+    else:
+        k, m = A.shape
+        n = B.shape[1]
+    _run_ws(_lib.gcn_gemm, (op, m, n, k, _ptr(A), _ld(A), _ptr(B), _ld(B), _ptr(out), _ld(out),
+                            _ptr(bias), epi, _ptr(mask), _ld(mask) if mask is not None else 0),
+            (P(_stream(stream)),), "gcn_gemm", ws, out.device)
+    return out
+
+
+def spmm(ptr, idx, val, B, out, stream=None):
+    nrows = ptr.numel() - 1
+    _check(_lib.gcn_spmm(nrows, _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B),
+                         _ld(B), _ptr(out), _ld(out), P(_stream(stream))), "gcn_spmm")
+    return out
+
+
+def column_sums(G, out, row_vals=None, mean=None, stream=None):
+    rows, w = G.shape
+    _run_ws(_lib.gcn_column_sums, (rows, w, _ptr(G), _ld(G), _ptr(out), _ptr(row_vals), _ptr(mean)),
+            (P(_stream(stream)),), "gcn_column_sums", None, G.device)
+    return out
+
+
+def adam(params, grads, ms, vs, step, lr=0.01, b1=0.9, b2=0.999, eps=1e-8, stream=None):
+    arr = (gcn_adam_tensor * len(params))()
+    for i, (p, g, m, v) in enumerate(zip(params, grads, ms, vs)):
+        arr[i] = gcn_adam_tensor(_ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel())
+    _check(_lib.gcn_adam(arr, len(params), step, lr, b1, b2, eps, P(_stream(stream))), "gcn_adam")
+
+
+def layer_order(f_in, f_out, index, act, x_sparse=False, order=ORDER_AUTO):
+    L = gcn_layer(f_in, f_out, pitch(f_in), pitch(f_out), act, order, index)
+    return _lib.gcn_layer_order(C.byref(L), int(x_sparse))
+
+
+def make_layer(f_in, f_out, ld_in, ld_out, act, index, order=ORDER_AUTO):
+    return gcn_layer(f_in, f_out, ld_in, ld_out, act, order, index)
+
+
+def layer_fwd(g: DeviceGraph, L: gcn_layer, Hin, x: SparseFeatures | None, W, b, Hout, saved=None,
+              labels=None, loss=None, logits=None, ws: _Workspace | None = None, stream=None):
+    dev = W.device
+    return _run_ws(_lib.gcn_layer_fwd,
+                   (C.byref(g.c), C.byref(L), _ptr(Hin), C.byref(x.c) if x is not None else None,
+                    _ptr(W), _ptr(b), _ptr(Hout), _ptr(saved), _ptr(labels), _ptr(loss), _ptr(logits)),
+                   (P(_stream(stream)),), "gcn_layer_fwd", ws, dev)
+
+
+def layer_bwd(g: DeviceGraph, L: gcn_layer, G, Hin, x: SparseFeatures | None, saved, W, dW, db,
+              Gprev=None, ws: _Workspace | None = None, stream=None):
+    dev = W.device
+    return _run_ws(_lib.gcn_layer_bwd,
+                   (C.byref(g.c), C.byref(L), _ptr(G), _ptr(Hin), C.byref(x.c) if x is not None else None,
+                    _ptr(saved), _ptr(W), _ptr(dW), _ptr(db), _ptr(Gprev)),
+                   (P(_stream(stream)),), "gcn_layer_bwd", ws, dev)
+
+
+# ---------------------------------------------------------------------------
+# whole model
+# ---------------------------------------------------------------------------
+
+
+class Model:
+    """Parameters, Adam state and activation buffers of an L-layer GCN on the device.
+
+    widths = (F, hidden..., classes).  Ws / bs: host arrays (fp32) of the initial
+    parameters.  x_sparse: layer 0 reads sparse X (its order is then transform-first).
+    """
+
+    def __init__(self, n, widths, Ws, bs, device="cuda", x_sparse=False, ld_x=None, lr=0.01,
+                 beta1=0.9, beta2=0.999, eps=1e-8, orders=None):
+        self.n = n
+        self.widths = tuple(widths)
+        L = len(widths) - 1
+        self.L = L
+        dev = torch.device(device)
+        self.layers = (gcn_layer * L)()
+        self.W, self.b, self.dW, self.db, self.mW, self.vW, self.mb, self.vb = ([] for _ in range(8))
+        self.act, self.saved, self.grad = [], [], []
+        for l in range(L):
+            fi, fo = widths[l], widths[l + 1]
+            ld_in = (ld_x if ld_x is not None else fi) if l == 0 else pitch(fi)
+            ld_out = pitch(fo)
+            act = ACT_SOFTMAX_CE if l == L - 1 else ACT_RELU
+            order = orders[l] if orders is not None else ORDER_AUTO
+            self.layers[l] = gcn_layer(fi, fo, ld_in, ld_out, act, order, l)
+            self.W.append(torch.as_tensor(Ws[l], dtype=torch.float32).to(dev).contiguous())
+            self.b.append(torch.as_tensor(bs[l], dtype=torch.float32).to(dev).contiguous())
+            self.dW.append(torch.zeros_like(self.W[-1]))
+            self.db.append(torch.zeros_like(self.b[-1]))
+            self.mW.append(torch.zeros_like(self.W[-1]))
+            self.vW.append(torch.zeros_like(self.W[-1]))
+            self.mb.append(torch.zeros_like(self.b[-1]))
+            self.vb.append(torch.zeros_like(self.b[-1]))
+            self.grad.append(padded(n, fo, dev))
+            if l < L - 1:
+                self.act.append(padded(n, fo, dev))
+            resolved = _lib.gcn_layer_order(C.byref(self.layers[l]), int(x_sparse and l == 0))
+            if resolved == AGGREGATE_FIRST:
+                self.saved.append(torch.zeros((n, ld_in), dtype=torch.float32, device=dev)[:, :fi])
+            else:
+                self.saved.append(None)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=dev)
+        self._ws = _Workspace()
+
+        def arr(ts):
+            a = (P * L)()
+            for i, t in enumerate(ts):
+                a[i] = _ptr(t) if t is not None else None
+            return a
+
+        acts = self.act + [None]
+        self._arrays = dict(W=arr(self.W), b=arr(self.b), dW=arr(self.dW), db=arr(self.db),
+                            mW=arr(self.mW), vW=arr(self.vW), mb=arr(self.mb), vb=arr(self.vb),
+                            act=arr(acts), saved=arr(self.saved), grad=arr(self.grad))
+        self.c = gcn_model()
+        self.c.n_layers = L
+        self.c.layers = self.layers
+        for k, v in self._arrays.items():
+            setattr(self.c, k, C.cast(v, C.POINTER(P)))
+        self.c.lr, self.c.beta1, self.c.beta2, self.c.eps, self.c.step = lr, beta1, beta2, eps, 0
+
+    @property
+    def step(self):
+        return self.c.step
+
+    def orders(self):
+        return [_lib.gcn_layer_order(C.byref(self.layers[l]), 0) for l in range(self.L)]
+
+    def epoch(self, g: DeviceGraph, X=None, x: SparseFeatures | None = None, labels=None, stream=None):
+        """One training epoch (asynchronous); returns the device loss tensor."""
+        _run_ws(_lib.gcn_epoch, (C.byref(self.c), C.byref(g.c), _ptr(X),
+                                 C.byref(x.c) if x is not None else None, _ptr(labels), _ptr(self.loss)),
+                (P(_stream(stream)),), "gcn_epoch", self._ws, self.loss.device)
+        return self.loss
+
+
+# ---------------------------------------------------------------------------
+# kernel timing
+# ---------------------------------------------------------------------------
+
+
+def profile_enable(capacity: int):
+    _check(_lib.gcn_profile_enable(capacity), "gcn_profile_enable")
+
+
+def profile_records():
+    out = []
+    for i in range(_lib.gcn_profile_count()):
+        r = gcn_profile_record()
+        _check(_lib.gcn_profile_read(i, C.byref(r)), "gcn_profile_read")
+        out.append(dict(name=r.name.decode(), width=r.width, rows=r.rows, nnz=r.nnz, ms=r.ms))
+    return out
+
+
+def profile_reset():
+    _check(_lib.gcn_profile_reset(), "gcn_profile_reset")
+
+
+def raw_lib():
+    """The loaded ctypes library (for ABI tests)."""
+    return _lib

@@ -1,0 +1,154 @@
+"""The C ABI without a GPU: exports, struct layout, host-side argument validation.
+
+Every call made here returns from host validation (or the workspace size
+query) before any HIP call, so it runs on a machine without a device.
+"""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gcn.h")
+
+
+@pytest.fixture(scope="module")
+def G():
+    import paper_2512_01678_amd.gcn as G
+    return G
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gcn_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(G):
+    names = declared_functions()
+    assert len(names) >= 17
+    out = subprocess.run(["nm", "-D", "--defined-only", G.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r" T (gcn_[a-z_]+)$", out, flags=re.M))
+    missing = [n for n in names if n not in exported]
+    assert not missing, missing
+    for n in names:
+        getattr(G.raw_lib(), n)
+
+
+def test_struct_layout_matches_c(G, tmp_path):
+    structs = {
+        "gcn_graph": G.gcn_graph, "gcn_sparse_x": G.gcn_sparse_x, "gcn_feature_info": G.gcn_feature_info,
+        "gcn_layer": G.gcn_layer, "gcn_model": G.gcn_model, "gcn_adam_tensor": G.gcn_adam_tensor,
+        "gcn_profile_record": G.gcn_profile_record,
+    }
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "gcn.h"', "int main(void) {"]
+    for sname, cls in structs.items():
+        lines.append(f'printf("{sname} size %zu\\n", sizeof({sname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'printf("{sname} {fname} %zu\\n", offsetof({sname}, {fname}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    "-D__HIP_PLATFORM_AMD__", str(src), "-o", str(exe)], check=True)
+    got = {}
+    for line in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines():
+        s, f, v = line.split()
+        got[(s, f)] = int(v)
+    for sname, cls in structs.items():
+        assert got[(sname, "size")] == C.sizeof(cls), sname
+        for fname, _ in cls._fields_:
+            assert got[(sname, fname)] == getattr(cls, fname).offset, (sname, fname)
+
+
+def test_status_strings(G):
+    L = G.raw_lib()
+    assert L.gcn_status_string(0) == b"GCN_OK"
+    assert L.gcn_status_string(-4) == b"GCN_E_CAPACITY"
+    assert L.gcn_status_string(-99) == b"GCN_E_UNKNOWN"
+    assert L.gcn_version() >= 1
+
+
+def test_host_validation_rejects_bad_calls(G):
+    L = G.raw_lib()
+    nb = G.sz(0)
+    # negative sizes
+    assert L.gcn_build_csr(-1, 0, None, None, None, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_build_csr(5, 1 << 30, None, None, None, None, C.byref(nb), None) == G.E_OVERFLOW
+    # workspace size query needs no device
+    assert L.gcn_build_csr(1000, 5000, None, None, None, None, C.byref(nb), None) == G.OK
+    assert nb.value > 4 * (2 * 5000 + 1000)
+    # ws_bytes NULL
+    assert L.gcn_build_csr(10, 5, None, None, None, None, None, None) == G.E_INVALID
+    # a workspace that is too small is a capacity error, before any launch
+    small = G.sz(8)
+    g = G.gcn_graph(10, 0, 100, 1, 1, 1, 1)
+    assert L.gcn_build_csr(10, 5, 1, 1, C.byref(g), 1, C.byref(small), None) == G.E_CAPACITY
+    assert "needed" in L.gcn_last_error().decode()
+    # feature stats: bad tau, pitch < width, bad force mode
+    info = G.gcn_feature_info()
+    assert L.gcn_feature_stats(1, 10, 8, 8, 4, 0, -1, None, C.byref(info), None, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_feature_stats(1, 10, 8, 7, 4, 5, -1, None, C.byref(info), None, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_feature_stats(1, 10, 8, 8, 4, 5, 7, None, C.byref(info), None, None, C.byref(nb), None) == G.E_INVALID
+    # gemm: unknown op, pitch too small, NULL operand
+    assert L.gcn_gemm(9, 4, 4, 4, 1, 4, 1, 4, 1, 4, None, 0, None, 0, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_gemm(G.OP_NN, 4, 4, 8, 1, 4, 1, 4, 1, 4, None, 0, None, 0, None, C.byref(nb), None) == G.E_INVALID
+    nb2 = G.sz(1 << 20)
+    assert L.gcn_gemm(G.OP_NN, 4, 4, 4, None, 4, 1, 4, 1, 4, None, 0, None, 0, 1, C.byref(nb2), None) == G.E_INVALID
+    # aggregate: NULL graph, mask epilogue without mask
+    assert L.gcn_aggregate(None, 4, 1, 4, None, 0, None, 0, 1, 4, None) == G.E_INVALID
+    g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1)
+    assert L.gcn_aggregate(C.byref(g2), 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(g2), 4, 1, 3, None, 0, None, 0, 1, 4, None) == G.E_INVALID
+    # adam: step 0, too many tensors
+    assert L.gcn_adam(None, 0, 0, 0.01, 0.9, 0.999, 1e-8, None) == G.E_INVALID
+    arr = (G.gcn_adam_tensor * 17)()
+    assert L.gcn_adam(arr, 17, 1, 0.01, 0.9, 0.999, 1e-8, None) == G.E_UNSUPPORTED
+    # profile read out of range
+    rec = G.gcn_profile_record()
+    assert L.gcn_profile_read(0, C.byref(rec)) == G.E_INVALID
+
+
+def test_layer_validation(G):
+    L = G.raw_lib()
+    nb = G.sz(0)
+    g = G.gcn_graph(10, 20, 20, 1, 1, 1, 1)
+    lay = G.gcn_layer(8, 4, 8, 4, G.ACT_RELU, G.ORDER_AUTO, 1)
+    # neither / both inputs
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(lay), None, None, 1, 1, 1, None, None, None, None, None,
+                           C.byref(nb), None) == G.E_INVALID
+    # pitch smaller than width
+    bad = G.gcn_layer(8, 4, 7, 4, G.ACT_RELU, G.ORDER_AUTO, 1)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(bad), 1, None, 1, 1, 1, None, None, None, None, None,
+                           C.byref(nb), None) == G.E_INVALID
+    # softmax without labels
+    sm = G.gcn_layer(8, 4, 8, 4, G.ACT_SOFTMAX_CE, G.ORDER_AUTO, 1)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(sm), 1, None, 1, 1, 1, None, None, None, None, None,
+                           C.byref(nb), None) == G.E_INVALID
+    # aggregate-first needs a saved buffer
+    af = G.gcn_layer(8, 64, 8, 64, G.ACT_RELU, G.AGGREGATE_FIRST, 1)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(af), 1, None, 1, 1, 1, None, None, None, None, None,
+                           C.byref(nb), None) == G.E_INVALID
+    # a valid transform-first layer: size query succeeds and covers the n x pitch(f_out) scratch
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(lay), 1, None, 1, 1, 1, None, None, None, None, None,
+                           C.byref(nb), None) == G.OK
+    assert nb.value >= 10 * 4 * 4
+    # backward: sparse input cannot have an input gradient
+    sx = G.gcn_sparse_x(10, 8, 5, 1, 1, 1, 1, 1, 1)
+    assert L.gcn_layer_bwd(C.byref(g), C.byref(lay), 1, None, C.byref(sx), None, 1, 1, 1, 1, None,
+                           C.byref(nb), None) == G.E_INVALID
+
+
+def test_order_rule(G):
+    # aggregate-first iff f_in * (1 + [l > 0]) < 2 f_out, dense input, not the loss layer
+    assert G.layer_order(128, 256, 0, G.ACT_RELU) == G.AGGREGATE_FIRST     # arxiv-like layer 0
+    assert G.layer_order(100, 256, 0, G.ACT_RELU) == G.AGGREGATE_FIRST     # products-like layer 0
+    assert G.layer_order(256, 256, 1, G.ACT_RELU) == G.TRANSFORM_FIRST
+    assert G.layer_order(602, 256, 0, G.ACT_RELU) == G.TRANSFORM_FIRST     # reddit-like layer 0
+    assert G.layer_order(128, 256, 0, G.ACT_RELU, x_sparse=True) == G.TRANSFORM_FIRST
+    assert G.layer_order(16, 700, 1, G.ACT_SOFTMAX_CE) == G.TRANSFORM_FIRST
+    assert G.layer_order(128, 256, 0, G.ACT_RELU, order=G.TRANSFORM_FIRST) == G.TRANSFORM_FIRST

@@ -1,0 +1,312 @@
+"""GPU parity of the individual steps against the fp64 oracle, through the C ABI.
+
+Integer / index work (CSR build, degrees, dinv, nonzero counts, compressed
+feature views) must match bit for bit; fp32 results must stay within 1e-4 of
+the oracle relative to each element's magnitude scale (sum of |terms|).
+"""
+import numpy as np
+import pytest
+import torch
+
+import gcn_synth as gs
+from helpers import adversarial_graphs, assert_mag_close, messy
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2512_01678_amd.gcn as G
+    return G
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def pitched(a, ld):
+    """Device copy of a (rows x w) with row pitch ld (extra columns filled with NaN)."""
+    rows, w = a.shape
+    buf = torch.full((rows, ld), float("nan"), dtype=torch.float32, device="cuda")
+    buf[:, :w] = dev(a.astype(np.float32))
+    return buf[:, :w]
+
+
+# ---------------------------------------------------------------------------
+# a1: A + I in CSR
+# ---------------------------------------------------------------------------
+
+
+def check_graph_equal(dg, og, n):
+    assert dg.nnz == og.nnz
+    np.testing.assert_array_equal(host(dg.row_ptr), og.row_ptr)
+    np.testing.assert_array_equal(host(dg.col_idx)[:og.nnz], og.col_idx)
+    np.testing.assert_array_equal(host(dg.deg)[:n], og.deg)
+    np.testing.assert_array_equal(host(dg.dinv)[:n].view(np.int32), og.dinv.view(np.int32))
+
+
+@pytest.mark.parametrize("case", adversarial_graphs(), ids=lambda c: c[0])
+def test_build_csr_bit_exact(G, orc, case):
+    name, n, s, d = case
+    print(f"[csr] {name} n={n} edges={s.size}", flush=True)
+    check_graph_equal(G.build_csr(n, dev(s), dev(d)), orc.build_csr(n, s, d), n)
+
+
+@pytest.mark.parametrize("name", ["cora_like", "arxiv_like"])
+def test_build_csr_workloads(G, orc, name):
+    wl = gs.WORKLOADS[name]
+    s, d = gs.make_graph(wl)
+    print(f"[csr] {name} n={wl.n} edges={s.size}", flush=True)
+    check_graph_equal(G.build_csr(wl.n, dev(s), dev(d)), orc.build_csr(wl.n, s, d), wl.n)
+
+
+def test_build_csr_rmat_small(G, orc):
+    s, d = gs.rmat(14, 1 << 18)
+    check_graph_equal(G.build_csr(1 << 14, dev(s), dev(d)), orc.build_csr(1 << 14, s, d), 1 << 14)
+
+
+def test_build_csr_rejects_out_of_range(G):
+    s = np.array([0, 1, 5], np.int32)
+    d = np.array([1, 2, 0], np.int32)
+    with pytest.raises(G.GcnError) as ei:
+        G.build_csr(5, dev(s), dev(d))
+    assert ei.value.status == G.E_RANGE
+    with pytest.raises(G.GcnError):
+        G.build_csr(5, dev(np.array([-1], np.int32)), dev(np.array([0], np.int32)))
+
+
+# ---------------------------------------------------------------------------
+# a2: density probe, decision, X_csr / X_csc
+# ---------------------------------------------------------------------------
+
+
+def feature_cases():
+    rng = np.random.default_rng(77)
+    special = rng.standard_normal((50, 70)).astype(np.float32)
+    special[rng.random((50, 70)) < 0.6] = 0.0
+    special[3, 4] = -0.0
+    special[5, 6] = np.nan
+    special[7, 8] = np.inf
+    special[9, :] = 0.0
+    thr = np.zeros((40, 25), np.float32)
+    thr.flat[: 40 * 25 // 5] = 1.5
+    rng.shuffle(thr.reshape(-1))
+    return [
+        ("cora_like", gs.make_features(gs.WORKLOADS["cora_like"])),
+        ("nonneg10", gs.features_bernoulli(2500, 4096, 0.1, binary=False)),
+        ("nonneg0.1", gs.features_bernoulli(3000, 1000, 0.001, binary=False)),
+        ("special", special),
+        ("zeros", np.zeros((33, 17), np.float32)),
+        ("ones", np.ones((33, 17), np.float32)),
+        ("identity", np.eye(64, 40, dtype=np.float32)),
+        ("threshold", thr),
+        ("one_col", (rng.random((1100, 1)) < 0.5).astype(np.float32)),
+        ("f65", (rng.random((2100, 65)) < 0.2).astype(np.float32) * 2.0),
+    ]
+
+
+@pytest.mark.parametrize("case", feature_cases(), ids=lambda c: c[0])
+def test_feature_stats_bit_exact(G, orc, case):
+    name, X = case
+    n, f = X.shape
+    print(f"[features] {name} {n}x{f}", flush=True)
+    nnz, rn = orc.feature_counts(X)
+    mode = orc.sparse_decision(nnz, n, f)
+    Xd = pitched(X, G.pitch(f) + 4)
+    rnd = torch.zeros(n, dtype=torch.int64, device="cuda")
+    info, sx = G.feature_stats(Xd, materialize=True, row_nnz=rnd)
+    assert info["nnz"] == nnz and info["mode"] == mode
+    assert info["sparsity"] == pytest.approx(orc.sparsity(nnz, n, f), abs=1e-15)
+    np.testing.assert_array_equal(host(rnd), rn)
+    rp, col, val = orc.dense_to_csr(X)
+    np.testing.assert_array_equal(host(sx.row_ptr), rp)
+    np.testing.assert_array_equal(host(sx.col)[:nnz], col)
+    np.testing.assert_array_equal(host(sx.val)[:nnz].view(np.int32), val.view(np.int32))
+    cp, row, cval = orc.dense_to_csc(X)
+    np.testing.assert_array_equal(host(sx.col_ptr), cp)
+    np.testing.assert_array_equal(host(sx.row)[:nnz], row)
+    np.testing.assert_array_equal(host(sx.cval)[:nnz].view(np.int32), cval.view(np.int32))
+
+
+def test_feature_decision_tau_and_force(G, orc):
+    X = np.zeros((40, 25), np.float32)
+    X.flat[: 40 * 25 // 5 + 1] = 1.0
+    info, _ = G.feature_stats(dev(X), materialize=False)
+    assert info["mode"] == G.DENSE
+    info, _ = G.feature_stats(dev(X), tau=(3, 4), materialize=False)
+    assert info["mode"] == G.SPARSE
+    info, _ = G.feature_stats(dev(X), force_mode=G.SPARSE, materialize=False)
+    assert info["mode"] == G.SPARSE
+
+
+# ---------------------------------------------------------------------------
+# a4 / a7: normalised aggregation (all widths, both pitches, epilogues)
+# ---------------------------------------------------------------------------
+
+WIDTHS = [1, 2, 3, 4, 5, 7, 8, 15, 16, 17, 31, 32, 33, 40, 41, 47, 63, 64, 65, 100, 127, 128, 129,
+          256, 257, 602]
+
+
+@pytest.fixture(scope="module")
+def agg_graph(G, orc):
+    rng = np.random.default_rng(5)
+    s1, d1 = gs.chung_lu(3000, 20000, seed=3)
+    s2 = np.zeros(5000, np.int32) + 7
+    d2 = rng.integers(0, 3000, 5000).astype(np.int32)     # one hub of degree ~2600
+    s = np.concatenate([s1, s2])
+    d = np.concatenate([d1, d2])
+    return orc.build_csr(3000, s, d), G.build_csr(3000, dev(s), dev(d))
+
+
+@pytest.mark.parametrize("w", WIDTHS)
+@pytest.mark.parametrize("vec", [True, False])
+def test_aggregate_widths(G, orc, agg_graph, w, vec):
+    og, dg = agg_graph
+    rng = np.random.default_rng(w)
+    n = og.n
+    M = rng.standard_normal((n, w)).astype(np.float32)
+    b = rng.standard_normal(w).astype(np.float32)
+    ld = G.pitch(w) if vec else w
+    Md = pitched(M, ld)
+    Zd = pitched(np.zeros((n, w), np.float32), ld)
+    mask = rng.standard_normal((n, w)).astype(np.float32)
+    Z, mag = orc.aggregate(og, M, b, want_mag=True)
+    for epi in (G.EPI_NONE, G.EPI_RELU, G.EPI_MASK):
+        G.aggregate(dg, Md, Zd, bias=dev(b), epi=epi, mask=pitched(mask, ld) if epi == G.EPI_MASK else None)
+        want = Z if epi == G.EPI_NONE else (np.maximum(Z, 0) if epi == G.EPI_RELU else Z * (mask > 0))
+        assert_mag_close(host(Zd), want, mag, f"aggregate w={w} ld={ld} epi={epi}")
+    # padding columns were never written
+    if ld > w:
+        assert torch.isnan(Zd.as_strided((n, ld), (ld, 1))[:, w:]).all()
+
+
+def test_aggregate_no_bias_deterministic(G, orc, agg_graph):
+    og, dg = agg_graph
+    M = np.random.default_rng(0).standard_normal((og.n, 256)).astype(np.float32)
+    Md = dev(M)
+    a = torch.empty_like(Md)
+    b = torch.empty_like(Md)
+    G.aggregate(dg, Md, a)
+    G.aggregate(dg, Md, b)
+    assert torch.equal(a, b)
+    Z, mag = orc.aggregate(og, M, want_mag=True)
+    assert_mag_close(host(a), Z, mag, "aggregate w=256 no bias")
+
+
+# ---------------------------------------------------------------------------
+# a3 (sparse), a8 (sparse): X_csr W and X_csc Q
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("f,w,p", [(1433, 16, 0.013), (4096, 128, 0.01), (500, 7, 0.2), (300, 33, 0.05)])
+def test_sparse_feature_products(G, orc, f, w, p):
+    n = 2708
+    X = gs.features_bernoulli(n, f, p, seed=1, binary=False)
+    rng = np.random.default_rng(f)
+    W = rng.standard_normal((f, w)).astype(np.float32)
+    Q = rng.standard_normal((n, w)).astype(np.float32)
+    _, sx = G.feature_stats(dev(X), materialize=True)
+    out = torch.empty((n, w), dtype=torch.float32, device="cuda")
+    G.spmm(sx.row_ptr, sx.col[:sx.nnz], sx.val[:sx.nnz], dev(W), out)
+    rp, col, val = orc.dense_to_csr(X)
+    ref, mag = orc.spmm(rp, col, val, W, want_mag=True)
+    assert_mag_close(host(out), ref, mag, f"X_csr W f={f} w={w}")
+    dW = torch.empty((f, w), dtype=torch.float32, device="cuda")
+    G.spmm(sx.col_ptr, sx.row[:sx.nnz], sx.cval[:sx.nnz], dev(Q), dW)
+    cp, row, cval = orc.dense_to_csc(X)
+    ref, mag = orc.spmm(cp, row, cval, Q, want_mag=True)
+    assert_mag_close(host(dW), ref, mag, f"X_csc Q f={f} w={w}")
+
+
+# ---------------------------------------------------------------------------
+# a3 / a5 / a8 / a9: matrix-core GEMMs
+# ---------------------------------------------------------------------------
+
+GEMM_SHAPES = [(1000, 256, 128), (1000, 40, 256), (777, 47, 256), (513, 7, 16), (300, 128, 602),
+               (333, 256, 256), (65, 16, 1433), (2049, 41, 41), (1, 1, 1), (100, 300, 5)]
+
+
+@pytest.mark.parametrize("op", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("shape", GEMM_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_gemm(G, op, shape):
+    m, n, k = shape
+    rng = np.random.default_rng(m * 7 + n * 3 + k)
+    A = rng.standard_normal((m, k)).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    bias = rng.standard_normal(n).astype(np.float32)
+    mask = rng.standard_normal((m, n)).astype(np.float32)
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    mag = np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64))
+    if op == "NN":
+        Ad, Bd, code = pitched(A, G.pitch(k) + 4), pitched(B, G.pitch(n)), G.OP_NN
+    elif op == "NT":
+        Ad, Bd, code = pitched(A, k), pitched(np.ascontiguousarray(B.T), G.pitch(k)), G.OP_NT
+    else:
+        Ad, Bd, code = pitched(np.ascontiguousarray(A.T), G.pitch(m)), pitched(B, n), G.OP_TN
+    C = pitched(np.zeros((m, n), np.float32), G.pitch(n) + 8)
+    G.gemm(code, Ad, Bd, C, bias=dev(bias))
+    assert_mag_close(host(C), ref + bias, mag + np.abs(bias), f"gemm {op} {shape}")
+    if op != "TN":
+        G.gemm(code, Ad, Bd, C, bias=dev(bias), epi=G.EPI_RELU)
+        assert_mag_close(host(C), np.maximum(ref + bias, 0), mag + np.abs(bias), f"gemm {op} relu")
+        G.gemm(code, Ad, Bd, C, epi=G.EPI_MASK, mask=dev(mask))
+        assert_mag_close(host(C), ref * (mask > 0), mag, f"gemm {op} mask")
+
+
+@pytest.mark.parametrize("m,n,k", [(128, 256, 169343), (256, 40, 50000), (100, 256, 70001), (602, 41, 20000),
+                                   (4096, 128, 4000), (16, 7, 2708)])
+def test_gemm_tn_long_reduction(G, m, n, k):
+    rng = np.random.default_rng(k)
+    A = rng.standard_normal((k, m)).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    ref = A.T.astype(np.float64) @ B.astype(np.float64)
+    mag = np.abs(A.T.astype(np.float64)) @ np.abs(B.astype(np.float64))
+    C = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    G.gemm(G.OP_TN, dev(A), dev(B), C)
+    C1 = host(C).copy()
+    assert_mag_close(C1, ref, mag, f"gemm TN {m}x{n}x{k}")
+    G.gemm(G.OP_TN, dev(A), dev(B), C)
+    np.testing.assert_array_equal(host(C), C1)  # fixed-order split-k reduction
+
+
+# ---------------------------------------------------------------------------
+# bias gradient / loss mean, Adam
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("rows,w", [(169343, 256), (2708, 7), (1000, 300), (5, 1), (0, 3)])
+def test_column_sums(G, rows, w):
+    rng = np.random.default_rng(rows + w)
+    Gm = rng.standard_normal((rows, w)).astype(np.float32)
+    rv = rng.random(rows).astype(np.float32)
+    out = torch.empty(max(w, 1), dtype=torch.float32, device="cuda")
+    mean = torch.empty(1, dtype=torch.float32, device="cuda")
+    G.column_sums(pitched(Gm, G.pitch(w)), out[:w], row_vals=dev(rv) if rows else None,
+                  mean=mean if rows else None)
+    want = Gm.astype(np.float64).sum(0)
+    mag = np.abs(Gm.astype(np.float64)).sum(0)
+    assert_mag_close(host(out)[:w], want, mag, "column sums")
+    if rows:
+        assert host(mean)[0] == pytest.approx(rv.astype(np.float64).mean(), rel=1e-6)
+
+
+def test_adam(G, orc):
+    rng = np.random.default_rng(3)
+    shapes = [(128, 256), (256,), (256, 40), (40,), (7,)]
+    ps = [rng.standard_normal(s).astype(np.float32) for s in shapes]
+    gs_ = [rng.standard_normal(s).astype(np.float32) for s in shapes]
+    ms = [rng.standard_normal(s).astype(np.float32) * 0.1 for s in shapes]
+    vs = [rng.random(s).astype(np.float32) * 0.01 for s in shapes]
+    dp, dg, dm, dv = ([dev(a) for a in arrs] for arrs in (ps, gs_, ms, vs))
+    G.adam(dp, dg, dm, dv, step=3)
+    for i in range(len(shapes)):
+        want, wm, wv = orc.adam(ps[i], gs_[i], ms[i], vs[i], 3)
+        np.testing.assert_allclose(host(dm[i]), wm, rtol=2e-6, atol=1e-7)
+        np.testing.assert_allclose(host(dv[i]), wv, rtol=2e-6, atol=1e-9)
+        assert_mag_close(host(dp[i]), want, np.abs(ps[i]) + 0.01, f"adam tensor {i}", rtol=1e-5)

@@ -1,0 +1,274 @@
+"""GPU parity of whole layers and epochs against the fp64 oracle, through the C ABI.
+
+Unit parity feeds the oracle the GPU's own layer inputs (so ReLU masks agree)
+and compares each output element against its magnitude scale; end-to-end
+parity runs the oracle from X alone and compares every tensor in the
+infinity norm (max error / max value <= 1e-4).
+"""
+import numpy as np
+import pytest
+import torch
+
+import gcn_synth as gs
+from helpers import assert_mag_close, assert_norm_close
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2512_01678_amd.gcn as G
+    return G
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def pad(G, a):
+    t = G.padded(a.shape[0], a.shape[1])
+    t.copy_(dev(a.astype(np.float32)))
+    return t
+
+
+class Problem:
+    def __init__(self, G, orc, wl, seed=0):
+        self.wl = wl
+        s, d = gs.make_graph(wl, seed)
+        self.og = orc.build_csr(wl.n, s, d)
+        self.dg = G.build_csr(wl.n, dev(s), dev(d))
+        self.X = gs.make_features(wl, seed)
+        self.y = gs.make_labels(wl, seed)
+        self.Ws, self.bs = gs.make_weights(wl, seed)
+
+
+@pytest.fixture(scope="module")
+def small(G, orc):
+    wl = gs.scaled(gs.WORKLOADS["arxiv_like"], 6000, 41000, name="arxiv_like_small")
+    return Problem(G, orc, wl)
+
+
+@pytest.fixture(scope="module")
+def cora(G, orc):
+    return Problem(G, orc, gs.WORKLOADS["cora_like"])
+
+
+def abs_agg(orc, og, A):
+    return orc.aggregate(og, np.abs(A))
+
+
+# ---------------------------------------------------------------------------
+# one layer forward / backward (unit parity)
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("order", ["TF", "AF"])
+@pytest.mark.parametrize("fi,fo,act", [(128, 256, "relu"), (256, 40, "softmax"), (100, 256, "relu"),
+                                       (41, 47, "none"), (256, 7, "softmax"), (602, 256, "relu")])
+def test_layer_forward(G, orc, small, order, fi, fo, act):
+    if order == "AF" and act == "softmax":
+        pytest.skip("aggregate-first is never chosen for the loss layer")
+    og, dg, n = small.og, small.dg, small.wl.n
+    rng = np.random.default_rng(fi + fo)
+    H = np.maximum(rng.standard_normal((n, fi)), 0).astype(np.float32)
+    W = (rng.standard_normal((fi, fo)) / np.sqrt(fi)).astype(np.float32)
+    b = rng.standard_normal(fo).astype(np.float32) * 0.1
+    y = rng.integers(0, fo, n).astype(np.int32)
+    code = {"relu": G.ACT_RELU, "none": G.ACT_NONE, "softmax": G.ACT_SOFTMAX_CE}[act]
+    L = G.make_layer(fi, fo, G.pitch(fi), G.pitch(fo), code, 1,
+                     G.TRANSFORM_FIRST if order == "TF" else G.AGGREGATE_FIRST)
+    Hd = pad(G, H)
+    out = G.padded(n, fo)
+    saved = G.padded(n, fi) if order == "AF" else None
+    loss = torch.zeros(1, device="cuda")
+    logits = G.padded(n, fo) if act == "softmax" else None
+    G.layer_fwd(dg, L, Hd, None, dev(W), dev(b), out, saved=saved, labels=dev(y), loss=loss, logits=logits)
+    Z = orc.aggregate(og, orc.matmul(H, W), b)
+    mag = orc.aggregate(og, orc.matmul(np.abs(H), np.abs(W)), np.abs(b))
+    if act == "relu":
+        assert_mag_close(host(out), np.maximum(Z, 0), mag, f"fwd {order} {fi}->{fo} relu")
+    elif act == "none":
+        assert_mag_close(host(out), Z, mag, f"fwd {order} {fi}->{fo}")
+    else:
+        assert_mag_close(host(logits), Z, mag, "logits")
+        lo, Gr, _ = orc.softmax_ce(Z, y)
+        assert host(loss)[0] == pytest.approx(lo, rel=1e-4)
+        assert_norm_close(host(out), Gr, "softmax-CE gradient")
+    if order == "AF":
+        P, pmag = orc.aggregate(og, H, want_mag=True)
+        assert_mag_close(host(saved), P, pmag, "saved A_hat H")
+
+
+@pytest.mark.parametrize("order", ["TF", "AF"])
+@pytest.mark.parametrize("fi,fo,first", [(256, 40, False), (128, 256, True), (256, 256, False), (47, 41, False)])
+def test_layer_backward(G, orc, small, order, fi, fo, first):
+    og, dg, n = small.og, small.dg, small.wl.n
+    rng = np.random.default_rng(fi * 3 + fo)
+    H = np.maximum(rng.standard_normal((n, fi)), 0).astype(np.float32)
+    W = (rng.standard_normal((fi, fo)) / np.sqrt(fi)).astype(np.float32)
+    Gr = (rng.standard_normal((n, fo)) / n).astype(np.float32)
+    L = G.make_layer(fi, fo, G.pitch(fi), G.pitch(fo), G.ACT_RELU, 0 if first else 1,
+                     G.TRANSFORM_FIRST if order == "TF" else G.AGGREGATE_FIRST)
+    Hd = pad(G, H)
+    saved = None
+    if order == "AF":
+        saved = G.padded(n, fi)
+        G.aggregate(dg, Hd, saved)
+    dW = torch.zeros((fi, fo), device="cuda")
+    db = torch.zeros(fo, device="cuda")
+    Gprev = None if first else G.padded(n, fi)
+    G.layer_bwd(dg, L, pad(G, Gr), Hd, None, saved, dev(W), dW, db, Gprev)
+    Q = orc.aggregate(og, Gr)
+    aQ = abs_agg(orc, og, Gr)
+    P = orc.aggregate(og, H)
+    if order == "TF":
+        dW_ref, dW_mag = orc.matmul(H.T, Q), orc.matmul(np.abs(H).T, aQ)
+    else:
+        dW_ref, dW_mag = orc.matmul(P.T, Gr), orc.matmul(np.abs(orc.aggregate(og, np.abs(H))).T, np.abs(Gr))
+    assert_mag_close(host(dW), dW_ref, dW_mag, f"dW {order}")
+    assert_mag_close(host(db), Gr.astype(np.float64).sum(0), np.abs(Gr.astype(np.float64)).sum(0), "db")
+    if Gprev is not None:
+        ref = orc.matmul(Q, W.T) * (H > 0)
+        mag = orc.matmul(aQ, np.abs(W).T)
+        assert_mag_close(host(Gprev), ref, mag, f"G_prev {order}")
+
+
+def test_layer_sparse_input(G, orc, cora):
+    og, dg, n = cora.og, cora.dg, cora.wl.n
+    X, W0, b0 = cora.X, cora.Ws[0], cora.bs[0] + 0.05
+    info, sx = G.feature_stats(dev(X))
+    assert info["mode"] == G.SPARSE
+    L = G.make_layer(1433, 16, 1433, G.pitch(16), G.ACT_RELU, 0)
+    out = G.padded(n, 16)
+    G.layer_fwd(dg, L, None, sx, dev(W0), dev(b0), out)
+    Z = orc.aggregate(og, orc.matmul(X, W0), b0)
+    mag = orc.aggregate(og, orc.matmul(np.abs(X), np.abs(W0)), np.abs(b0))
+    assert_mag_close(host(out), np.maximum(Z, 0), mag, "sparse layer-0 forward")
+    Gr = (np.random.default_rng(0).standard_normal((n, 16)) / n).astype(np.float32)
+    dW = torch.zeros((1433, 16), device="cuda")
+    db = torch.zeros(16, device="cuda")
+    G.layer_bwd(dg, L, pad(G, Gr), None, sx, None, dev(W0), dW, db, None)
+    Q = orc.aggregate(og, Gr)
+    assert_mag_close(host(dW), orc.matmul(X.T, Q), orc.matmul(np.abs(X).T, abs_agg(orc, og, Gr)),
+                     "sparse layer-0 dW")
+
+
+# ---------------------------------------------------------------------------
+# whole epochs (end-to-end parity, determinism)
+# ---------------------------------------------------------------------------
+
+
+def snapshot(m):
+    """The GPU model's parameters and Adam state, widened to fp64 on the host."""
+    return {k: [host(t) for t in getattr(m, k)] for k in ("W", "b", "mW", "vW", "mb", "vb")}
+
+
+def run_epochs(G, orc, p, epochs, sparse):
+    """Each epoch: the oracle starts from the GPU's own pre-epoch parameters and Adam
+    state, so every epoch is a well-conditioned comparison (Adam's first steps move
+    each weight by about lr * sign(g), which would amplify rounding in g if the two
+    trajectories were left to run apart)."""
+    n = p.wl.n
+    Xd = dev(p.X)
+    sx = None
+    if sparse:
+        info, sx = G.feature_stats(Xd)
+        assert info["mode"] == G.SPARSE
+    m = G.Model(n, p.wl.widths, p.Ws, p.bs, x_sparse=sparse, ld_x=p.wl.f)
+    yd = dev(p.y)
+    osx = orc.SparseX(p.X) if sparse else None
+    for t in range(1, epochs + 1):
+        st = snapshot(m)
+        m.epoch(p.dg, X=None if sparse else Xd, x=sx, labels=yd)
+        out = orc.epoch(p.og, p.X, p.y, st["W"], st["b"], st["mW"], st["vW"], st["mb"], st["vb"], t,
+                        sparse=osx)
+        tag = f"{p.wl.name} epoch {t}"
+        assert host(m.loss)[0] == pytest.approx(out["loss"], rel=1e-4), tag
+        for l in range(m.L):
+            assert_norm_close(host(m.grad[l]), out["Gs"][l], f"{tag} G_{l}")
+            assert_norm_close(host(m.dW[l]), out["dWs"][l], f"{tag} dW_{l}")
+            assert_norm_close(host(m.db[l]), out["dbs"][l], f"{tag} db_{l}")
+            if l < m.L - 1:
+                assert_norm_close(host(m.act[l]), out["Hs"][l + 1], f"{tag} H_{l + 1}")
+            # the Adam step, applied by the oracle to the GPU's own gradients
+            for nm, gnm, mnm, vnm in (("W", "dW", "mW", "vW"), ("b", "db", "mb", "vb")):
+                want, wm, wv = orc.adam(st[nm][l], host(getattr(m, gnm)[l]), st[mnm][l], st[vnm][l], t)
+                assert_mag_close(host(getattr(m, nm)[l]), want, np.abs(st[nm][l]) + 0.01,
+                                 f"{tag} Adam {nm}_{l}", rtol=1e-5)
+                np.testing.assert_allclose(host(getattr(m, mnm)[l]), wm, rtol=1e-5, atol=1e-12)
+                np.testing.assert_allclose(host(getattr(m, vnm)[l]), wv, rtol=1e-5, atol=1e-15)
+    return m
+
+
+def test_epochs_sparse_path_cora_like(G, orc, cora):
+    m = run_epochs(G, orc, cora, 3, sparse=True)
+    assert m.step == 3
+
+
+def test_epochs_dense_path_aggregate_first(G, orc, small):
+    m = run_epochs(G, orc, small, 2, sparse=False)
+    assert m.orders()[0] == G.AGGREGATE_FIRST and m.orders()[1] == G.TRANSFORM_FIRST
+
+
+def test_epochs_forced_dense_on_sparse_features(G, orc, cora):
+    run_epochs(G, orc, cora, 2, sparse=False)
+
+
+def test_epoch_bitwise_deterministic(G, small):
+    p = small
+    outs = []
+    for _ in range(2):
+        m = G.Model(p.wl.n, p.wl.widths, p.Ws, p.bs)
+        for _ in range(3):
+            m.epoch(p.dg, X=dev(p.X), labels=dev(p.y))
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in m.W + m.b + [m.loss]])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# full-size workload in the benchmark's launch configuration: sampled rows
+# ---------------------------------------------------------------------------
+
+
+def test_arxiv_like_full_size_sampled(G, orc):
+    wl = gs.WORKLOADS["arxiv_like"]
+    p = Problem(G, orc, wl)
+    n = wl.n
+    m = G.Model(n, wl.widths, p.Ws, p.bs, ld_x=wl.f)
+    Xd = dev(p.X)
+    yd = dev(p.y)
+    m.epoch(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    deg = p.og.deg
+    rows = np.unique(np.concatenate([rng.integers(0, n, 400), np.argsort(deg)[-20:]])).astype(np.int32)
+    Hs = [p.X.astype(np.float64)] + [host(a) for a in m.act]
+    # forward of every layer on the sampled rows, from the GPU's own layer inputs
+    for l in range(m.L - 1):
+        Wl, bl = p.Ws[l].astype(np.float64), p.bs[l].astype(np.float64)
+        Z = orc.aggregate(p.og, Hs[l] @ Wl, bl, rows=rows)
+        mag = orc.aggregate(p.og, np.abs(Hs[l]) @ np.abs(Wl), np.abs(bl), rows=rows)
+        assert_mag_close(Hs[l + 1][rows], np.maximum(Z, 0), mag, f"full-size H_{l + 1} rows")
+    # loss layer, all rows (needed for the mean)
+    Zl = orc.aggregate(p.og, Hs[-1] @ p.Ws[-1].astype(np.float64), p.bs[-1])
+    lo, Gl, _ = orc.softmax_ce(Zl, p.y)
+    assert host(m.loss)[0] == pytest.approx(lo, rel=1e-4)
+    assert_norm_close(host(m.grad[-1]), Gl, "full-size G_last")
+    # backward of every layer from the GPU's own G_l
+    for l in range(m.L - 1, -1, -1):
+        Gg = host(m.grad[l])
+        Q = orc.aggregate(p.og, Gg)
+        aQ = orc.aggregate(p.og, np.abs(Gg))
+        assert_mag_close(host(m.dW[l]), Hs[l].T @ Q, np.abs(Hs[l]).T @ aQ, f"full-size dW_{l}")
+        if l > 0:
+            ref = (Q[rows] @ p.Ws[l].T.astype(np.float64)) * (Hs[l][rows] > 0)
+            mag = aQ[rows] @ np.abs(p.Ws[l].T.astype(np.float64))
+            assert_mag_close(host(m.grad[l - 1])[rows], ref, mag, f"full-size G_{l - 1} rows")
