@@ -1,0 +1,251 @@
+"""Benchmark: full-batch GCN training epochs per second on one MI355X.
+
+One step = one training epoch of the whole hot path (forward through every
+layer with the fused aggregation, softmax cross-entropy, backward, Adam) on a
+seeded synthetic graph resident in HBM.  Graph generation, upload, the CSR
+build and the density probe run once before timing (the paper also excludes
+one-time setup from its per-epoch times).
+
+Prints ONE JSON line.  Extra objects:
+  roofline      the dominant kernel family's algorithmic bytes (or flops) per
+                launch over its average launch time, from HIP events recorded
+                around every launch inside the timed region;
+  cpu_baseline  the fp64 oracle's epoch time on this host's cores (bounded sample).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GCN train epochs/sec (fwd+bwd) on 1 MI355X; SpMM achieved HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="arxiv_like")
+    ap.add_argument("--tau", default="4/5", help="sparse-path threshold tau as num/den")
+    ap.add_argument("--force-mode", default="auto", choices=["auto", "dense", "sparse"])
+    ap.add_argument("--cpu-baseline", default="auto", choices=["auto", "off"])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU work budget for the oracle leg")
+    ap.add_argument("--no-profile", action="store_true", help="no per-launch events (pure epoch timing)")
+    ap.add_argument("--copy-gib", type=float, default=0.0,
+                    help="instead of training, time a plain device copy of this many GiB "
+                         "(calibrates HBM counters against a kernel of known traffic)")
+    return ap.parse_args()
+
+
+def alg_bytes_aggregate(nnz: int, rows: int, w: int) -> int:
+    """Algorithmic bytes of one normalised aggregation at width w: neighbour-row gathers
+    4 nnz w, column indices 4 nnz, row offsets 8 (rows + 1), dinv 4 rows, output 4 rows w."""
+    return 4 * nnz * w + 4 * nnz + 8 * (rows + 1) + 4 * rows + 4 * rows * w
+
+
+def sha_of(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if the kernel
+    source is unchanged since the counters were taken; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        table = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    rec = table.get(f"{kernel}@{workload}")
+    if not rec:
+        return None
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src) or sha_of(src) != rec["source_sha256"]:
+        return None
+    return rec["bytes_per_launch"]
+
+
+def copy_calibration(gib: float):
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    reps = 10
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "ms": ms,
+                      "GBps": 2 * n * 4 / ms / 1e6}))
+
+
+def cpu_baseline(wl, s, d, X, y, Ws, bs, sparse: bool, budget_s: float):
+    """The oracle as it stands, timed on this host: full epochs of the same workload,
+    repeated until about budget_s seconds of work (at least one)."""
+    from oracle import oracle as orc
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    og = orc.build_csr(wl.n, s, d)
+    osx = orc.SparseX(X) if sparse else None
+    Wd = [w.astype(np.float64) for w in Ws]
+    bd = [b.astype(np.float64) for b in bs]
+    z = [np.zeros(w.shape) for w in Ws]
+    zb = [np.zeros(b.shape) for b in bs]
+    times = []
+    t_all = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        orc.epoch(og, X, y, Wd, bd, z, z, zb, zb, 1, sparse=osx)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_all >= budget_s or len(times) >= 50:
+            break
+    sec = float(np.median(times))
+    return {"value": 1.0 / sec, "unit": "epochs/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(times)} full fp64 oracle epoch(s) of {wl.name} (forward, loss, backward, "
+                      f"Adam), median {sec:.3f} s/epoch"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU path "
+              "is not built -- see DESIGN.md for how it would shard", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if args.copy_gib > 0:
+        copy_calibration(args.copy_gib)
+        return
+
+    import gcn_synth as gs
+    import paper_2512_01678_amd.gcn as G
+
+    wl = gs.WORKLOADS[args.workload]
+    t0 = time.perf_counter()
+    s, d = gs.make_graph(wl)
+    X = gs.make_features(wl)
+    y = gs.make_labels(wl)
+    Ws, bs = gs.make_weights(wl)
+    t_gen = time.perf_counter() - t0
+    print(f"[bench] {wl.name}: inputs generated in {t_gen:.1f} s", file=sys.stderr, flush=True)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ld_x = G.pitch(wl.f)
+    Xd = torch.zeros((wl.n, ld_x), dtype=torch.float32, device=dev)
+    Xd[:, :wl.f] = torch.from_numpy(X).to(dev)
+    Xv = Xd[:, :wl.f]
+    sd, dd = torch.from_numpy(s).to(dev), torch.from_numpy(d).to(dev)
+    yd = torch.from_numpy(y).to(dev)
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    g = G.build_csr(wl.n, sd, dd)
+    t_csr = time.perf_counter() - t0
+    tau = tuple(int(v) for v in args.tau.split("/"))
+    force = {"auto": -1, "dense": G.DENSE, "sparse": G.SPARSE}[args.force_mode]
+    t0 = time.perf_counter()
+    info, sx = G.feature_stats(Xv, tau=tau, force_mode=force)
+    t_probe = time.perf_counter() - t0
+    sparse = info["mode"] == G.SPARSE
+    print(f"[bench] nnz(A+I)={g.nnz} csr {t_csr * 1e3:.1f} ms; probe s={info['sparsity']:.4f} -> "
+          f"{'sparse' if sparse else 'dense'} ({t_probe * 1e3:.1f} ms)", file=sys.stderr, flush=True)
+    del sd, dd
+
+    m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x)
+    Xin = None if sparse else Xv
+    for _ in range(args.warmup):
+        m.epoch(g, X=Xin, x=sx, labels=yd)
+    torch.cuda.synchronize()
+    print(f"[bench] {args.warmup} warm-up epochs done", file=sys.stderr, flush=True)
+
+    launches_per_epoch = 64
+    if not args.no_profile:
+        G.profile_enable(launches_per_epoch * args.steps)
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    t_wall = time.perf_counter()
+    for _ in range(args.steps):
+        m.epoch(g, X=Xin, x=sx, labels=yd)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_total = ev0.elapsed_time(ev1)
+    ms_per_step = ms_total / args.steps
+    loss = float(m.loss.cpu()[0])
+    print(f"[bench] {args.steps} epochs: {ms_per_step:.3f} ms/epoch (wall {t_wall * 1e3 / args.steps:.3f}), "
+          f"loss {loss:.5f}", file=sys.stderr, flush=True)
+
+    # per-launch records -> per-family averages
+    fam = {}
+    if not args.no_profile:
+        for r in G.profile_records():
+            f = fam.setdefault(r["name"], dict(ms=0.0, count=0, width=r["width"], rows=r["rows"], nnz=r["nnz"]))
+            f["ms"] += r["ms"]
+            f["count"] += 1
+        G.profile_enable(0)
+    kernels = {}
+    for name, f in sorted(fam.items(), key=lambda kv: -kv[1]["ms"]):
+        avg = f["ms"] / f["count"]
+        k = {"avg_ms": round(avg, 5), "launches_per_epoch": f["count"] // args.steps,
+             "share": round(f["ms"] / ms_total, 4)}
+        if name.startswith("aggregate_w"):
+            by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
+            k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+        elif name.startswith("gemm_"):
+            mm, nn, kk = (int(v) for v in name.split("_")[2].split("x"))
+            k["TFLOPs"] = round(2 * mm * nn * kk / (avg * 1e-3) / 1e12, 2)
+        kernels[name] = k
+
+    roofline = None
+    agg = {k: v for k, v in fam.items() if k.startswith("aggregate_w")}
+    if agg:
+        # dominant kernel family: the aggregation launch with the largest total time
+        name, f = max(agg.items(), key=lambda kv: kv[1]["ms"])
+        avg_s = f["ms"] / f["count"] * 1e-3
+        by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
+        achieved = by / avg_s / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(name, wl.name),
+                    "kernel": name, "alg_bytes_per_launch": by, "avg_launch_ms": round(avg_s * 1e3, 5)}
+
+    cpu = None
+    if args.cpu_baseline == "auto":
+        print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, s, d, X, y, Ws, bs, sparse, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": round(1000.0 / ms_per_step, 3), "unit": "epochs/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "nodes": wl.n, "nnz_A_plus_I": g.nnz, "widths": list(wl.widths),
+                   "feature_path": "sparse" if sparse else "dense", "sparsity": round(info["sparsity"], 6),
+                   "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
+                   "per_launch_events": not args.no_profile},
+        "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
+        "setup_ms": {"csr_build": round(t_csr * 1e3, 2), "density_probe": round(t_probe * 1e3, 2)},
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

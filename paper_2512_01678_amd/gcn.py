@@ -322,6 +322,7 @@ class Model:
         self.widths = tuple(widths)
         L = len(widths) - 1
         self.L = L
+        self.x_sparse = bool(x_sparse)
         dev = torch.device(device)
         self.layers = (gcn_layer * L)()
         self.W, self.b, self.dW, self.db, self.mW, self.vW, self.mb, self.vb = ([] for _ in range(8))
@@ -374,7 +375,8 @@ class Model:
         return self.c.step
 
     def orders(self):
-        return [_lib.gcn_layer_order(C.byref(self.layers[l]), 0) for l in range(self.L)]
+        return [_lib.gcn_layer_order(C.byref(self.layers[l]), int(self.x_sparse and l == 0))
+                for l in range(self.L)]
 
     def epoch(self, g: DeviceGraph, X=None, x: SparseFeatures | None = None, labels=None, stream=None):
         """One training epoch (asynchronous); returns the device loss tensor."""
