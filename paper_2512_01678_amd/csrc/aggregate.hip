@@ -7,14 +7,16 @@
 //  * sparse-feature products (Section IV-B): w_e = val[e], s_u = 1 (X_csr W, X_csc G).
 //
 // Mapping (the paper's row-per-block idea of Algorithm 3, re-cut for 64-wide
-// wavefronts): a lane group of LANES lanes owns one output row; each lane owns
-// VEC consecutive columns, so one neighbour row is fetched by the whole group
-// as LANES coalesced 16-byte loads.  The group reads LANES column indices at a
-// time (one per lane), then walks them, broadcasting each index and weight
-// with a cross-lane shuffle and keeping UNR neighbour loads in flight before
-// the FMAs.  Accumulators stay in registers and every output element is
-// written once, so no atomics are involved and results are deterministic.
-// Narrow rows (w <= 128) pack 2..64 rows into one wavefront.
+// wavefronts): a slice of LANES lanes covers the row's columns, each lane VEC
+// consecutive columns, so one neighbour row is fetched as LANES coalesced
+// 16-byte loads.  A row is owned by `slots` such slices (LANES * slots <= 64
+// lanes); slice k takes neighbours k, k + slots, ...  The row's lanes read the
+// column indices cooperatively (one per lane), broadcast each index and weight
+// with a cross-lane shuffle, and keep UNR neighbour loads in flight before the
+// FMAs.  The slices are summed with cross-lane adds at the end.  Accumulators
+// stay in registers and every output element is written once, so no atomics
+// are involved and results are deterministic.  Narrow rows of low-degree
+// graphs pack several rows into one wavefront (slots = 1).
 #include "internal.h"
 
 namespace gcn {
@@ -36,6 +38,12 @@ struct Vec<4> {
   static __device__ __forceinline__ float get(const T& v, int i) {
     return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
   }
+  static __device__ __forceinline__ void add_xor(T& v, int o, int width) {
+    v.x += __shfl_xor(v.x, o, width);
+    v.y += __shfl_xor(v.y, o, width);
+    v.z += __shfl_xor(v.z, o, width);
+    v.w += __shfl_xor(v.w, o, width);
+  }
 };
 template <>
 struct Vec<1> {
@@ -44,6 +52,7 @@ struct Vec<1> {
   static __device__ __forceinline__ T zero() { return 0.f; }
   static __device__ __forceinline__ void fma(T& acc, float w, const T& x) { acc = fmaf(w, x, acc); }
   static __device__ __forceinline__ float get(const T& v, int) { return v; }
+  static __device__ __forceinline__ void add_xor(T& v, int o, int width) { v += __shfl_xor(v, o, width); }
 };
 
 template <int LANES>
@@ -61,13 +70,18 @@ __device__ __forceinline__ float group_sum(float v) {
 
 constexpr int kBlock = 256;
 
+// One row per group of LANES * slots lanes (slots is a power of two, LANES * slots <= 64).
+// Each of the `slots` lane slices walks every slots-th neighbour of the row; the slices
+// are summed at the end with cross-lane adds in a fixed pattern (deterministic).
 template <int LANES, int VEC, int EPI, bool USE_VAL>
-__global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
+__global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
   using V = Vec<VEC>;
-  constexpr int GROUPS = kBlock / LANES;
-  constexpr int UNR = LANES >= 8 ? 8 : LANES;
-  const int lane = threadIdx.x & (LANES - 1);
-  const int64_t row = (int64_t)blockIdx.x * GROUPS + threadIdx.x / LANES;
+  constexpr int UNR = LANES >= 4 ? 8 : 4;
+  const int gw = LANES * slots;
+  const int lig = threadIdx.x & (gw - 1);
+  const int slot = lig / LANES;
+  const int lane = lig & (LANES - 1);
+  const int64_t row = (int64_t)blockIdx.x * (kBlock / gw) + threadIdx.x / gw;
   const bool live = row < p.n;
   const int c0 = (blockIdx.y * LANES + lane) * VEC;
   const bool cok = live && c0 < p.w;
@@ -79,36 +93,35 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
   }
   typename V::T acc = V::zero();
   const float* Mc = p.M + c0;
-  for (int64_t base = beg; base < end; base += LANES) {
-    const int cnt = (int)((end - base) < LANES ? (end - base) : LANES);
+  for (int64_t base = beg; base < end; base += gw) {
+    const int cnt = (int)((end - base) < gw ? (end - base) : gw);
     int my_j = 0;
     float my_w = 0.f;
-    if (lane < cnt) {
-      my_j = p.col[base + lane];
-      my_w = USE_VAL ? p.val[base + lane] : p.dinv[my_j];
+    if (lig < cnt) {
+      my_j = p.col[base + lig];
+      my_w = USE_VAL ? p.val[base + lig] : p.dinv[my_j];
     }
-    int t = 0;
-    for (; t + UNR <= cnt; t += UNR) {
+    for (int t = 0; t < cnt; t += slots * UNR) {
       int jj[UNR];
       float ww[UNR];
+      bool ok[UNR];
       typename V::T xs[UNR];
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
-        jj[u] = __shfl(my_j, t + u, LANES);
-        ww[u] = __shfl(my_w, t + u, LANES);
+        const int e = t + u * slots + slot;
+        ok[u] = e < cnt;
+        const int src = ok[u] ? e : 0;
+        jj[u] = __shfl(my_j, src, gw);
+        ww[u] = __shfl(my_w, src, gw);
       }
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) xs[u] = cok ? V::load(Mc + (int64_t)jj[u] * p.ldm) : V::zero();
+      for (int u = 0; u < UNR; ++u) xs[u] = (ok[u] && cok) ? V::load(Mc + (int64_t)jj[u] * p.ldm) : V::zero();
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) V::fma(acc, ww[u], xs[u]);
-    }
-    for (; t < cnt; ++t) {
-      const int j = __shfl(my_j, t, LANES);
-      const float wv = __shfl(my_w, t, LANES);
-      const typename V::T x = cok ? V::load(Mc + (int64_t)j * p.ldm) : V::zero();
-      V::fma(acc, wv, x);
+      for (int u = 0; u < UNR; ++u) V::fma(acc, ok[u] ? ww[u] : 0.f, xs[u]);
     }
   }
+  // sum the slices: after this every slice holds the full row
+  for (int o = LANES; o < gw; o <<= 1) V::add_xor(acc, o, gw);
   if (!live) return;
 
   const float s = USE_VAL ? 1.f : p.dinv[row];
@@ -121,7 +134,7 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
   }
 
   if constexpr (EPI == AGG_SOFTMAX) {
-    // whole logits row is held by this lane group (w <= LANES * VEC)
+    // whole logits row is held by each slice (w <= LANES * VEC); slice 0 writes
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < VEC; ++i)
@@ -141,6 +154,7 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
     for (int i = 0; i < VEC; ++i)
       if (c0 + i == y) zy = z[i];
     zy = group_sum<LANES>(zy);
+    if (slot != 0) return;
     if (lane == 0) p.row_loss[row] = (logf(se) + mx) - zy;
     const float inv_se = 1.f / se;
     float* out = p.Z + row * p.ldz;
@@ -155,7 +169,7 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
     }
     return;
   } else {
-    if (!cok) return;
+    if (!cok || slot != 0) return;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
       if constexpr (EPI == AGG_RELU) z[i] = fmaxf(z[i], 0.f);
@@ -177,37 +191,56 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p) {
 }
 
 template <int LANES, int VEC, int EPI>
-gcn_status launch3(const AggParams& p, hipStream_t s) {
-  constexpr int GROUPS = kBlock / LANES;
-  dim3 grid((unsigned)ceil_div(p.n, GROUPS), (unsigned)ceil_div(p.w, LANES * VEC));
-  if (p.val)
-    hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, true>), grid, dim3(kBlock), 0, s, p);
-  else
-    hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, false>), grid, dim3(kBlock), 0, s, p);
+gcn_status launch3(const AggParams& p, int slots, hipStream_t s) {
+  const int gw = LANES * slots;
+  dim3 grid((unsigned)ceil_div(p.n, kBlock / gw), (unsigned)ceil_div(p.w, LANES * VEC));
+  if constexpr (EPI == AGG_NONE) {
+    if (p.val) {
+      hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, true>), grid, dim3(kBlock), 0, s, p, slots);
+      return check_launch("spmm");
+    }
+  }
+  hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, false>), grid, dim3(kBlock), 0, s, p, slots);
   return check_launch("aggregate");
 }
 
 template <int LANES, int VEC>
-gcn_status launch2(const AggParams& p, hipStream_t s) {
+gcn_status launch2(const AggParams& p, int slots, hipStream_t s) {
   switch (p.epi) {
-    case AGG_NONE: return launch3<LANES, VEC, AGG_NONE>(p, s);
-    case AGG_RELU: return launch3<LANES, VEC, AGG_RELU>(p, s);
-    case AGG_MASK: return launch3<LANES, VEC, AGG_MASK>(p, s);
-    default: return launch3<LANES, VEC, AGG_SOFTMAX>(p, s);
+    case AGG_NONE: return launch3<LANES, VEC, AGG_NONE>(p, slots, s);
+    case AGG_RELU: return launch3<LANES, VEC, AGG_RELU>(p, slots, s);
+    case AGG_MASK: return launch3<LANES, VEC, AGG_MASK>(p, slots, s);
+    default: return launch3<LANES, VEC, AGG_SOFTMAX>(p, slots, s);
   }
 }
 
 template <int VEC>
-gcn_status launch1(const AggParams& p, int lanes, hipStream_t s) {
+gcn_status launch1(const AggParams& p, int lanes, int slots, hipStream_t s) {
   switch (lanes) {
-    case 1: return launch2<1, VEC>(p, s);
-    case 2: return launch2<2, VEC>(p, s);
-    case 4: return launch2<4, VEC>(p, s);
-    case 8: return launch2<8, VEC>(p, s);
-    case 16: return launch2<16, VEC>(p, s);
-    case 32: return launch2<32, VEC>(p, s);
-    default: return launch2<64, VEC>(p, s);
+    case 1: return launch2<1, VEC>(p, slots, s);
+    case 2: return launch2<2, VEC>(p, slots, s);
+    case 4: return launch2<4, VEC>(p, slots, s);
+    case 8: return launch2<8, VEC>(p, slots, s);
+    case 16: return launch2<16, VEC>(p, slots, s);
+    case 32: return launch2<32, VEC>(p, slots, s);
+    default: return launch2<64, VEC>(p, slots, s);
   }
+}
+
+// Neighbour slices per row: as many as keep at least 2 neighbours per slice on an
+// average row (slices beyond that would mostly idle), within one wavefront.
+int pick_slots(int lanes, int64_t nnz, int64_t rows) {
+  const int max_slots = std::min(64 / lanes, 16);
+  if (const char* e = getenv("GCN_AGG_SLOTS")) {
+    int v = atoi(e), s = 1;
+    while (s * 2 <= v && s * 2 <= max_slots) s *= 2;
+    return s;
+  }
+  if (nnz < 0 || rows <= 0) return 1;
+  const double avg = (double)nnz / (double)rows;
+  int s = 1;
+  while (s * 2 <= max_slots && 2.0 * (s * 2) <= avg) s *= 2;
+  return s;
 }
 
 }  // namespace
@@ -222,10 +255,11 @@ gcn_status launch_aggregate(const AggParams& p, int64_t nnz, hipStream_t s) {
   while (lanes < need && lanes < 64) lanes <<= 1;
   if (p.epi == AGG_SOFTMAX && need > lanes)
     return fail(GCN_E_UNSUPPORTED, "softmax epilogue needs width <= 256 (vector) or 64 (scalar)");
+  const int slots = pick_slots(lanes, nnz, p.n);
   char name[64];
   snprintf(name, sizeof name, "%s_w%d", p.val ? "spmm" : "aggregate", p.w);
   ProfScope prof(name, p.w, p.n, nnz, s);
-  return vec4 ? launch1<4>(p, lanes, s) : launch1<1>(p, lanes, s);
+  return vec4 ? launch1<4>(p, lanes, slots, s) : launch1<1>(p, lanes, slots, s);
 }
 
 }  // namespace gcn

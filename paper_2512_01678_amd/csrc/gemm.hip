@@ -31,6 +31,8 @@ struct GemmArgs {
   int64_t kchunk;  // k extent per split
   int a_vec;       // A rows are 16-byte aligned with pitch % 4 == 0
   int b_vec;
+  int o_vec;       // output rows (C, or the split-k partials) likewise
+  int m_vec;       // mask rows likewise
 };
 
 // Load 4 consecutive elements src[i .. i+3] (i < lim are valid) into v.
@@ -100,8 +102,13 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   constexpr int KH = BK / 2;
   using SA = Stage<BM, BK, NT, !TA>;  // A(m,k): k-contiguous unless transposed
   using SB = Stage<BN, BK, NT, TB>;   // B(k,n): n-contiguous unless transposed
-  __shared__ __attribute__((aligned(16))) float lds_a[2][SA::kLdsFloats];
-  __shared__ __attribute__((aligned(16))) float lds_b[2][SB::kLdsFloats];
+  constexpr int kA = SA::kLdsFloats, kB = SB::kLdsFloats;
+  constexpr int RB = BM / WM;               // rows of one epilogue round
+  constexpr int kEpi = RB * (BN + kPad);
+  constexpr int kTot = 2 * (kA + kB) > kEpi ? 2 * (kA + kB) : kEpi;
+  __shared__ __attribute__((aligned(16))) float smem[kTot];
+  auto lds_a = [&](int b) { return smem + b * kA; };
+  auto lds_b = [&](int b) { return smem + 2 * kA + b * kB; };
 
   const GemmParams& p = g.p;
   const int tid = threadIdx.x;
@@ -135,15 +142,15 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   const int64_t nslab = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   if (nslab > 0) {
     load_slab(kbeg);
-    sa.store(lds_a[0], tid);
-    sb.store(lds_b[0], tid);
+    sa.store(lds_a(0), tid);
+    sb.store(lds_b(0), tid);
   }
   __syncthreads();
   for (int64_t s = 0; s < nslab; ++s) {
     const int buf = (int)(s & 1);
     if (s + 1 < nslab) load_slab(kbeg + (s + 1) * BK);
-    const float* la = lds_a[buf];
-    const float* lb = lds_b[buf];
+    const float* la = lds_a(buf);
+    const float* lb = lds_b(buf);
     float af[TM][KH], bf[TN][KH];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -161,50 +168,102 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
     if (s + 1 < nslab) {
-      sa.store(lds_a[buf ^ 1], tid);
-      sb.store(lds_b[buf ^ 1], tid);
+      sa.store(lds_a(buf ^ 1), tid);
+      sb.store(lds_b(buf ^ 1), tid);
     }
     __syncthreads();
   }
 
-  // epilogue: lane l32 holds column l32 of each 32x32 sub-tile; register r holds
-  // row 8*(r/4) + 4*h + r%4.
+  // Epilogue, one wave-row of the tile (RB rows) per round: the waves of that row
+  // put their accumulators in LDS (lane l32 holds column l32 of a 32x32 sub-tile,
+  // register r row 8*(r/4) + 4*h + r%4), then the whole workgroup streams the RB x BN
+  // slab out as row-contiguous 16-byte accesses (mask, bias, C or the split-k partial).
+  float* const tile = smem;
+  const int64_t ldo = SPLIT ? p.n : p.ldc;
+  float* const out = SPLIT ? g.part + (int64_t)blockIdx.z * p.m * p.n : p.C;
+  const bool ovec = g.o_vec;
+  const bool mvec = g.m_vec;
+  for (int round = 0; round < WM; ++round) {
+    if (wm == round) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int64_t col = n0 + wn * (BN / WN) + j * 32 + l32;
-      if (col >= p.n) continue;
-      const float bv = (!SPLIT && p.bias) ? p.bias[col] : 0.f;
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * (BM / WM) + i * 32 + 8 * (r / 4) + 4 * h + (r % 4);
-        if (row >= p.m) continue;
-        float v = acc[i][j][r];
-        if (SPLIT) {
-          g.part[((int64_t)blockIdx.z * p.m + row) * p.n + col] = v;
-        } else {
-          v += bv;
-          if (EPI == GEMM_RELU) v = fmaxf(v, 0.f);
-          if (EPI == GEMM_MASK) v = p.mask[row * p.ldmask + col] > 0.f ? v : 0.f;
-          p.C[row * p.ldc + col] = v;
+          for (int r = 0; r < 16; ++r)
+            tile[(i * 32 + 8 * (r / 4) + 4 * h + (r % 4)) * (BN + kPad) + wn * (BN / WN) + j * 32 + l32] =
+                acc[i][j][r];
+    }
+    __syncthreads();
+    constexpr int kChunks = RB * BN / 4;
+    for (int c = tid; c < kChunks; c += NT) {
+      const int rr = c / (BN / 4), cq = (c % (BN / 4)) * 4;
+      const int64_t row = m0 + (int64_t)round * RB + rr;
+      const int64_t col = n0 + cq;
+      if (row >= p.m || col >= p.n) continue;
+      float v[4];
+      const float4 t4 = *reinterpret_cast<const float4*>(tile + rr * (BN + kPad) + cq);
+      v[0] = t4.x; v[1] = t4.y; v[2] = t4.z; v[3] = t4.w;
+      const bool full = col + 4 <= p.n;
+      if (!SPLIT) {
+        float mk[4] = {1.f, 1.f, 1.f, 1.f};
+        if (EPI == GEMM_MASK) {
+          const float* mp = p.mask + row * p.ldmask + col;
+          if (mvec && full) {
+            const float4 m4 = *reinterpret_cast<const float4*>(mp);
+            mk[0] = m4.x; mk[1] = m4.y; mk[2] = m4.z; mk[3] = m4.w;
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) mk[q] = col + q < p.n ? mp[q] : 0.f;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (p.bias && col + q < p.n) v[q] += p.bias[col + q];
+          if (EPI == GEMM_RELU) v[q] = fmaxf(v[q], 0.f);
+          if (EPI == GEMM_MASK) v[q] = mk[q] > 0.f ? v[q] : 0.f;
         }
       }
+      float* op = out + row * ldo + col;
+      if (ovec && full) {
+        *reinterpret_cast<float4*>(op) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (col + q < p.n) op[q] = v[q];
+      }
     }
+    __syncthreads();
   }
 }
 
-// C(m,n) = sum_s part[s](m,n) (+ bias) in split order.
+// C(m,n) = sum_s part[s](m,n) (+ bias).  A workgroup owns 64 consecutive output
+// elements; its 4 split lanes sum the partials s = lane, lane + 4, ... in increasing
+// order and are then combined in lane order, so the rounding is fixed.
 __global__ void __launch_bounds__(256) k_splitk_reduce(const float* part, int64_t splits, int64_t m,
                                                        int64_t n, float* C, int64_t ldc,
                                                        const float* bias) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= m * n) return;
-  const int64_t row = i / n, col = i % n;
-  float s = 0.f;
-  for (int64_t z = 0; z < splits; ++z) s += part[z * m * n + i];
-  if (bias) s += bias[col];
-  C[row * ldc + col] = s;
+  __shared__ float red[4][64];
+  const int e = threadIdx.x % 64, sl = threadIdx.x / 64;
+  const int64_t i = (int64_t)blockIdx.x * 64 + e;
+  const int64_t mn = m * n;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  if (i < mn) {
+    int64_t z = sl;
+    for (; z + 12 < splits; z += 16) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] += part[(z + 4 * u) * mn + i];
+    }
+    for (; z < splits; z += 4) acc[0] += part[z * mn + i];
+  }
+  red[sl][e] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  __syncthreads();
+  if (sl == 0 && i < mn) {
+    float s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+    const int64_t row = i / n, col = i % n;
+    if (bias) s += bias[col];
+    C[row * ldc + col] = s;
+  }
 }
 
 struct Shape {
@@ -219,8 +278,9 @@ Shape pick_shape(const GemmParams& p) {
 
 int64_t pick_splits(const GemmParams& p, Shape sh) {
   if (!p.ta) return 1;  // only A^T B reduces over the long (row) dimension
+  // about 1024 workgroups, each walking at least 256 rows of k
   const int64_t tiles = ceil_div(p.m, sh.bm) * ceil_div(p.n, sh.bn);
-  int64_t s = ceil_div(2048, tiles);
+  int64_t s = ceil_div(1024, tiles);
   const int64_t max_s = ceil_div(p.k, 256);
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;
@@ -273,6 +333,8 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   g.kchunk = round_up(ceil_div(p.k, splits), 16);
   g.a_vec = p.lda % 4 == 0 && aligned16(p.A);
   g.b_vec = p.ldb % 4 == 0 && aligned16(p.B);
+  g.o_vec = splits > 1 ? (p.n % 4 == 0 && aligned16(g.part)) : (p.ldc % 4 == 0 && aligned16(p.C));
+  g.m_vec = p.epi == GEMM_MASK && p.ldmask % 4 == 0 && aligned16(p.mask);
   char name[64];
   snprintf(name, sizeof name, "gemm_%s%s_%ldx%ldx%ld", p.ta ? "T" : "N", p.tb ? "T" : "N",
            (long)p.m, (long)p.n, (long)p.k);
@@ -284,7 +346,7 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   else st = launch_layout<true, true>(g, sh, splits, s);
   if (st != GCN_OK || splits == 1) return st;
   const int64_t total = p.m * p.n;
-  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, s, g.part,
+  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, g.part,
                      splits, p.m, p.n, p.C, p.ldc, p.bias);
   return check_launch("gemm split-k reduce");
 }
@@ -293,63 +355,110 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
 // column sums (bias gradient) and mean of per-row values (loss), fixed order
 // ---------------------------------------------------------------------------
 namespace {
-constexpr int kColBlocks = 512;
-constexpr int kColThreads = 256;
+constexpr int kColBlocksMax = 1024;
 
-// Block b sums rows [b*chunk, (b+1)*chunk): thread (c, r4) takes columns c, c+64, ...
-// and rows r4, r4+4, ...; the 4 row lanes are combined in LDS in index order.
-__global__ void __launch_bounds__(kColThreads) k_colsum_partial(int64_t rows, int32_t w,
-                                                                const float* G, int64_t ldg,
-                                                                int64_t chunk, const float* rv,
-                                                                double* part, int32_t pw) {
-  __shared__ double red[4][64];
-  const int c = threadIdx.x % 64, r4 = threadIdx.x / 64;
+int col_blocks(int64_t rows) { return (int)std::max<int64_t>(1, std::min<int64_t>(kColBlocksMax, ceil_div(rows, 64))); }
+
+// Workgroup b sums rows [b*chunk, (b+1)*chunk).  Thread (c4, rl): columns 4*c4 .. 4*c4+3
+// of each 256-column slab, rows rl, rl+4, ...; the 4 row lanes are combined in order.
+__global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w, const float* G, int64_t ldg,
+                                                        int64_t chunk, const float* rv, double* part,
+                                                        int32_t pw, int vec) {
+  __shared__ double red[4][256];
+  const int c4 = threadIdx.x % 64, rl = threadIdx.x / 64;
   const int64_t r0 = (int64_t)blockIdx.x * chunk;
   const int64_t r1 = r0 + chunk < rows ? r0 + chunk : rows;
-  for (int cb = 0; cb < pw; cb += 64) {
-    const int col = cb + c;
-    double s = 0.0;
-    if (col < w) {
-      for (int64_t r = r0 + r4; r < r1; r += 4) s += (double)G[r * ldg + col];
-    } else if (col == w && rv) {
-      for (int64_t r = r0 + r4; r < r1; r += 4) s += (double)rv[r];
+  for (int cb = 0; cb < w; cb += 256) {
+    const int c = cb + 4 * c4;
+    float a[4] = {0.f, 0.f, 0.f, 0.f}, b[4] = {0.f, 0.f, 0.f, 0.f};
+    if (c < w) {
+      if (vec && c + 4 <= w) {
+        int64_t r = r0 + rl;
+        for (; r + 4 < r1; r += 8) {
+          const float4 x = *reinterpret_cast<const float4*>(G + r * ldg + c);
+          const float4 y = *reinterpret_cast<const float4*>(G + (r + 4) * ldg + c);
+          a[0] += x.x; a[1] += x.y; a[2] += x.z; a[3] += x.w;
+          b[0] += y.x; b[1] += y.y; b[2] += y.z; b[3] += y.w;
+        }
+        if (r < r1) {
+          const float4 x = *reinterpret_cast<const float4*>(G + r * ldg + c);
+          a[0] += x.x; a[1] += x.y; a[2] += x.z; a[3] += x.w;
+        }
+      } else {
+        for (int64_t r = r0 + rl; r < r1; r += 4)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (c + i < w) a[i] += G[r * ldg + c + i];
+      }
     }
-    red[r4][c] = s;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[rl][4 * c4 + i] = (double)a[i] + (double)b[i];
     __syncthreads();
-    if (r4 == 0 && col < pw) part[(int64_t)blockIdx.x * pw + col] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    if (rl == 0) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (c + i < w)
+          part[(int64_t)blockIdx.x * pw + c + i] =
+              ((red[0][4 * c4 + i] + red[1][4 * c4 + i]) + red[2][4 * c4 + i]) + red[3][4 * c4 + i];
+    }
     __syncthreads();
+  }
+  if (rv) {
+    double s = 0.0;
+    for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) s += (double)rv[r];
+    red[0][threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+      if ((int)threadIdx.x < o) red[0][threadIdx.x] += red[0][threadIdx.x + o];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) part[(int64_t)blockIdx.x * pw + w] = red[0][0];
   }
 }
 
-__global__ void __launch_bounds__(256) k_colsum_final(const double* part, int nblk, int32_t w,
-                                                      int32_t pw, float* out, float* mean,
-                                                      double inv_rows) {
-  for (int col = threadIdx.x; col < pw; col += 256) {
-    double s = 0.0;
-    for (int b = 0; b < nblk; ++b) s += part[(int64_t)b * pw + col];
+// out[c] = sum_b part[b][c]: 64 columns per workgroup, 4 lanes over b (b = lane mod 4,
+// increasing), combined in lane order.
+__global__ void __launch_bounds__(256) k_colsum_final(const double* part, int nblk, int32_t w, int32_t pw,
+                                                      float* out, float* mean, double inv_rows) {
+  __shared__ double red[4][64];
+  const int cl = threadIdx.x % 64, bl = threadIdx.x / 64;
+  const int col = blockIdx.x * 64 + cl;
+  double s0 = 0.0, s1 = 0.0;
+  if (col < pw) {
+    int b = bl;
+    for (; b + 4 < nblk; b += 8) {
+      s0 += part[(int64_t)b * pw + col];
+      s1 += part[(int64_t)(b + 4) * pw + col];
+    }
+    if (b < nblk) s0 += part[(int64_t)b * pw + col];
+  }
+  red[bl][cl] = s0 + s1;
+  __syncthreads();
+  if (bl == 0 && col < pw) {
+    const double s = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
     if (col < w) out[col] = (float)s;
-    else if (mean && col == w) *mean = (float)(s * inv_rows);
+    else if (mean) *mean = (float)(s * inv_rows);
   }
 }
 }  // namespace
 
 size_t colsum_workspace(int64_t rows, int32_t w) {
-  (void)rows;
-  return sizeof(double) * (size_t)kColBlocks * (size_t)(w + 1);
+  return sizeof(double) * (size_t)col_blocks(rows) * (size_t)(w + 1);
 }
 
 gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, float* out,
                          const float* row_vals, float* mean, void* ws, hipStream_t s) {
   const int32_t pw = w + (row_vals ? 1 : 0);
   if (pw == 0) return GCN_OK;
-  const int64_t chunk = rows > 0 ? ceil_div(rows, kColBlocks) : 1;
-  const int nblk = kColBlocks;
+  const int nblk = col_blocks(rows);
+  const int64_t chunk = rows > 0 ? ceil_div(rows, nblk) : 1;
   double* part = static_cast<double*>(ws);
-  hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(kColThreads), 0, s, rows, w, G, ldg, chunk,
-                     row_vals, part, pw);
+  const int vec = G && ldg % 4 == 0 && aligned16(G);
+  hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
+                     part, pw, vec);
   GCN_TRY(check_launch("column sums"));
-  hipLaunchKernelGGL(k_colsum_final, dim3(1), dim3(256), 0, s, part, nblk, w, pw, out, mean,
-                     rows > 0 ? 1.0 / (double)rows : 0.0);
+  hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 64)), dim3(256), 0, s, part, nblk, w, pw,
+                     out, mean, rows > 0 ? 1.0 / (double)rows : 0.0);
   return check_launch("column sums final");
 }
 
