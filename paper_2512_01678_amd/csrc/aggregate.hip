@@ -156,16 +156,25 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
     zy = group_sum<LANES>(zy);
     if (slot != 0) return;
     if (lane == 0) p.row_loss[row] = (logf(se) + mx) - zy;
+    if (!cok) return;
     const float inv_se = 1.f / se;
-    float* out = p.Z + row * p.ldz;
-    float* lg = p.logits ? p.logits + row * p.ldl : nullptr;
+    float gv[VEC];
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) {
-      const int c = c0 + i;
-      if (c < p.w) {
-        out[c] = (e[i] * inv_se - (c == y ? 1.f : 0.f)) * p.inv_n;
-        if (lg) lg[c] = z[i];
-      }
+    for (int i = 0; i < VEC; ++i) gv[i] = (e[i] * inv_se - (c0 + i == y ? 1.f : 0.f)) * p.inv_n;
+    float* out = p.Z + row * p.ldz + c0;
+    float* lg = p.logits ? p.logits + row * p.ldl + c0 : nullptr;
+    if (VEC == 4 && c0 + 4 <= p.w) {
+      *reinterpret_cast<float4*>(out) = make_float4(gv[0], gv[VEC > 1 ? 1 : 0], gv[VEC > 2 ? 2 : 0],
+                                                    gv[VEC > 3 ? 3 : 0]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i)
+        if (c0 + i < p.w) out[i] = gv[i];
+    }
+    if (lg) {
+#pragma unroll
+      for (int i = 0; i < VEC; ++i)
+        if (c0 + i < p.w) lg[i] = z[i];
     }
     return;
   } else {

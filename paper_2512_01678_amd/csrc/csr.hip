@@ -88,13 +88,25 @@ __global__ void k_fill(int32_t n, int64_t ne, const int32_t* src, const int32_t*
   }
 }
 
-__global__ void k_classify(int32_t n, const int32_t* cnt, int32_t* lists, int32_t* flags) {
+// Row lists by length class; one atomic per class per wavefront (ballot-aggregated).
+__global__ void __launch_bounds__(256) k_classify(int32_t n, const int32_t* cnt, int32_t* lists, int32_t* flags) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int32_t len = cnt[i];
-  const int cls = len <= kSmall ? 0 : (len <= kMedium ? 1 : 2);
-  const int32_t pos = atomicAdd(&flags[1 + cls], 1);
-  lists[(int64_t)cls * n + pos] = (int32_t)i;
+  const int lane = threadIdx.x % 64;
+  int cls = -1;
+  if (i < n) {
+    const int32_t len = cnt[i];
+    cls = len <= kSmall ? 0 : (len <= kMedium ? 1 : 2);
+  }
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  for (int c = 0; c < 3; ++c) {
+    const uint64_t bal = __ballot(cls == c);
+    if (!bal) continue;
+    const int leader = __ffsll((unsigned long long)bal) - 1;
+    int32_t base = 0;
+    if (lane == leader) base = atomicAdd(&flags[1 + c], (int32_t)__popcll(bal));
+    base = __shfl(base, leader);
+    if (cls == c) lists[(int64_t)c * n + base + (int32_t)__popcll(bal & below)] = (int32_t)i;
+  }
 }
 
 // one wavefront per row of <= 64 entries

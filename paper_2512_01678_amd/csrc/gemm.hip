@@ -416,28 +416,27 @@ __global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w,
   }
 }
 
-// out[c] = sum_b part[b][c]: 64 columns per workgroup, 4 lanes over b (b = lane mod 4,
-// increasing), combined in lane order.
+// out[c] = sum_b part[b][c]: 8 columns per workgroup, 32 lanes per column; lane q
+// sums b = q, q + 32, ... in increasing order, then the 32 lane sums are combined by
+// a fixed binary tree.
 __global__ void __launch_bounds__(256) k_colsum_final(const double* part, int nblk, int32_t w, int32_t pw,
                                                       float* out, float* mean, double inv_rows) {
-  __shared__ double red[4][64];
-  const int cl = threadIdx.x % 64, bl = threadIdx.x / 64;
-  const int col = blockIdx.x * 64 + cl;
-  double s0 = 0.0, s1 = 0.0;
-  if (col < pw) {
-    int b = bl;
-    for (; b + 4 < nblk; b += 8) {
-      s0 += part[(int64_t)b * pw + col];
-      s1 += part[(int64_t)(b + 4) * pw + col];
-    }
-    if (b < nblk) s0 += part[(int64_t)b * pw + col];
-  }
-  red[bl][cl] = s0 + s1;
+  __shared__ double red[32][8];
+  const int cl = threadIdx.x % 8, q = threadIdx.x / 8;
+  const int col = blockIdx.x * 8 + cl;
+  double s = 0.0;
+  if (col < pw)
+    for (int b = q; b < nblk; b += 32) s += part[(int64_t)b * pw + col];
+  red[q][cl] = s;
   __syncthreads();
-  if (bl == 0 && col < pw) {
-    const double s = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
-    if (col < w) out[col] = (float)s;
-    else if (mean) *mean = (float)(s * inv_rows);
+  for (int o = 16; o > 0; o >>= 1) {
+    if (q < o) red[q][cl] += red[q + o][cl];
+    __syncthreads();
+  }
+  if (q == 0 && col < pw) {
+    const double t = red[0][cl];
+    if (col < w) out[col] = (float)t;
+    else if (mean) *mean = (float)(t * inv_rows);
   }
 }
 }  // namespace
@@ -457,7 +456,7 @@ gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, f
   hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
                      part, pw, vec);
   GCN_TRY(check_launch("column sums"));
-  hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 64)), dim3(256), 0, s, part, nblk, w, pw,
+  hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 8)), dim3(256), 0, s, part, nblk, w, pw,
                      out, mean, rows > 0 ? 1.0 / (double)rows : 0.0);
   return check_launch("column sums final");
 }
