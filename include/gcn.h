@@ -66,6 +66,30 @@ const char* gcn_last_error(void);
 int32_t gcn_version(void);
 
 /*
+ * Row-split plan for long rows of a compressed matrix (graph hubs, or columns of
+ * X in its CSC view).  A row with more than GCN_SPLIT_MIN entries is "long": it is
+ * cut into chunks of GCN_SPLIT_CHUNK entries (the last may be shorter); the
+ * product kernels sum each chunk separately and then add a long row's chunk sums
+ * in chunk order, so a hub costs many short work items instead of one long one
+ * and the result stays deterministic.  The plan is filled by gcn_build_csr (for
+ * the graph) and gcn_feature_stats (for the CSC view) when `rows` is non-NULL;
+ * a zeroed plan (rows == NULL) means "no splitting".  rows, owner and order hold
+ * `cap` entries and first holds cap + 1.  A long row of len > 2 * GCN_SPLIT_CHUNK
+ * entries has ceil(len / GCN_SPLIT_CHUNK) < 1.5 len / GCN_SPLIT_CHUNK chunks, so
+ * cap >= 3 * entries / (2 * GCN_SPLIT_CHUNK) + 1 always suffices.
+ */
+enum { GCN_SPLIT_MIN = 4096, GCN_SPLIT_CHUNK = 2048 };
+typedef struct gcn_split {
+  int32_t n_long;     /* long rows */
+  int64_t n_chunk;    /* chunks over all long rows */
+  int64_t cap;        /* capacity of the arrays below (entries) */
+  int32_t* rows;      /* device, n_long: long row ids, ascending */
+  int64_t* first;     /* device, n_long + 1: first chunk of each long row; first[n_long] = n_chunk */
+  int32_t* owner;     /* device, n_chunk: index into rows of each chunk */
+  int64_t* order;     /* device, n_chunk, or NULL: order in which chunks are processed */
+} gcn_split;
+
+/*
  * Graph operator A_hat in CSR form.  Row i lists the distinct neighbours of
  * node i plus i itself, columns ascending; deg[i] is the row length and
  * dinv[i] = (float)(1 / sqrt((double)deg[i])).  Entry (i, j) of A_hat is
@@ -79,6 +103,7 @@ typedef struct gcn_graph {
   int32_t* col_idx;   /* device, nnz_cap */
   int32_t* deg;       /* device, n */
   float* dinv;        /* device, n */
+  gcn_split split;    /* hub rows (optional; see gcn_split) */
 } gcn_graph;
 
 /*
@@ -95,6 +120,7 @@ typedef struct gcn_sparse_x {
   int64_t* col_ptr;   /* device, f + 1; NULL: no CSC view */
   int32_t* row;       /* device, nnz */
   float* cval;        /* device, nnz */
+  gcn_split csc_split;  /* long columns of the CSC view (optional; see gcn_split) */
 } gcn_sparse_x;
 
 /* Density probe result (Section IV-B). */
@@ -121,7 +147,8 @@ typedef struct gcn_layer {
  * u != v adds u-v in both directions; pairs with u == v are ignored; repeated
  * pairs count once; each node gets one self-loop.  On entry g->n, g->nnz_cap
  * and the four device pointers must be set; nnz_cap = 2 n_edges + n always
- * suffices.  On return g->nnz holds the entry count.
+ * suffices.  On return g->nnz holds the entry count.  When g->split.rows is
+ * non-NULL the hub split plan is built too (g->split.order is left NULL).
  * Errors: GCN_E_RANGE if an endpoint is outside [0, n) (outputs undefined),
  * GCN_E_CAPACITY if nnz > nnz_cap or the workspace is short.
  */
@@ -140,7 +167,11 @@ gcn_status gcn_build_csr(int32_t n, int64_t n_edges, const int32_t* d_src, const
  * overrides the decision; -1 keeps it.
  * When x != NULL it also materialises X_csr (DenseToCSR) and, if x->col_ptr
  * != NULL, X_csc (DenseToCSC); x->nnz must hold the capacity on entry and
- * holds nnz on return.  GCN_E_CAPACITY if the capacity is short.
+ * holds nnz on return.  GCN_E_CAPACITY if the capacity is short.  When
+ * x->csc_split.rows is non-NULL, the split plan of the CSC view's long columns is
+ * built, with x->csc_split.order (if non-NULL) set to process the chunks
+ * chunk-index-major (all columns' first chunks, then all second chunks, ...), so
+ * chunks that cover the same window of rows run together.
  */
 gcn_status gcn_feature_stats(const float* d_X, int32_t n, int32_t f, int64_t ldx,
                              int32_t tau_num, int32_t tau_den, int32_t force_mode,
@@ -236,11 +267,12 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
  * Algorithm 3's row-parallel, atomic-free aggregation).  Asynchronous.
  * d_M: n x w (pitch ldm).  d_bias: w or NULL.  epi: GCN_EPI_NONE, GCN_EPI_RELU
  * (max(Z, 0)) or GCN_EPI_MASK (Z * 1[mask > 0], d_mask n x w, pitch ldmask).
- * d_Z: n x w (pitch ldz); must not overlap d_M.
+ * d_Z: n x w (pitch ldz); must not overlap d_M.  The workspace holds the chunk
+ * sums of split hub rows (g->split.n_chunk x w floats, rounded up).
  */
 gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm,
                          const float* d_bias, int32_t epi, const float* d_mask, int64_t ldmask,
-                         float* d_Z, int64_t ldz, hipStream_t stream);
+                         float* d_Z, int64_t ldz, void* d_ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
  * gcn_gemm -- dense fp32 product on the matrix cores (the dense-path GEMM of
@@ -263,11 +295,13 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
  * i < nrows (Section IV-B backend-specialised primitives: X_csr W forward,
  * X^T G from X_csc backward).  Asynchronous.  d_ptr: nrows + 1 int64;
  * d_idx, d_val: d_ptr[nrows] entries with 0 <= idx < b_rows; d_B: b_rows x w
- * (pitch ldb); d_C: nrows x w (pitch ldc).
+ * (pitch ldb); d_C: nrows x w (pitch ldc).  split: plan of the long rows of this
+ * matrix (or NULL); the workspace holds their chunk sums.
  */
 gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, const float* d_val,
                     int64_t b_rows, int32_t w, const float* d_B, int64_t ldb, float* d_C,
-                    int64_t ldc, hipStream_t stream);
+                    int64_t ldc, const gcn_split* split, void* d_ws, size_t* ws_bytes,
+                    hipStream_t stream);
 
 /*
  * gcn_column_sums -- out[c] = sum_i G[i,c] (the bias gradient) and, when

@@ -17,6 +17,12 @@
 // stay in registers and every output element is written once, so no atomics
 // are involved and results are deterministic.  Narrow rows of low-degree
 // graphs pack several rows into one wavefront (slots = 1).
+//
+// Long rows (hubs; more than GCN_SPLIT_MIN entries) would leave one group
+// walking the whole row while the rest of the GPU idles.  With a split plan,
+// the main kernel skips them; k_chunks sums each GCN_SPLIT_CHUNK-entry chunk
+// into a partial row, and k_combine adds a long row's partials in chunk order
+// and applies the same epilogue.
 #include "internal.h"
 
 namespace gcn {
@@ -28,12 +34,19 @@ template <>
 struct Vec<4> {
   using T = float4;
   static __device__ __forceinline__ T load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ void store(float* p, const T& v) { *reinterpret_cast<float4*>(p) = v; }
   static __device__ __forceinline__ T zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
   static __device__ __forceinline__ void fma(T& acc, float w, const T& x) {
     acc.x = fmaf(w, x.x, acc.x);
     acc.y = fmaf(w, x.y, acc.y);
     acc.z = fmaf(w, x.z, acc.z);
     acc.w = fmaf(w, x.w, acc.w);
+  }
+  static __device__ __forceinline__ void add(T& acc, const T& x) {
+    acc.x += x.x;
+    acc.y += x.y;
+    acc.z += x.z;
+    acc.w += x.w;
   }
   static __device__ __forceinline__ float get(const T& v, int i) {
     return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
@@ -49,8 +62,10 @@ template <>
 struct Vec<1> {
   using T = float;
   static __device__ __forceinline__ T load(const float* p) { return *p; }
+  static __device__ __forceinline__ void store(float* p, const T& v) { *p = v; }
   static __device__ __forceinline__ T zero() { return 0.f; }
   static __device__ __forceinline__ void fma(T& acc, float w, const T& x) { acc = fmaf(w, x, acc); }
+  static __device__ __forceinline__ void add(T& acc, const T& x) { acc += x; }
   static __device__ __forceinline__ float get(const T& v, int) { return v; }
   static __device__ __forceinline__ void add_xor(T& v, int o, int width) { v += __shfl_xor(v, o, width); }
 };
@@ -70,36 +85,37 @@ __device__ __forceinline__ float group_sum(float v) {
 
 constexpr int kBlock = 256;
 
-// One row per group of LANES * slots lanes (slots is a power of two, LANES * slots <= 64).
-// Each of the `slots` lane slices walks every slots-th neighbour of the row; the slices
-// are summed at the end with cross-lane adds in a fixed pattern (deterministic).
-template <int LANES, int VEC, int EPI, bool USE_VAL>
-__global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
+// Lane geometry of a group of LANES * slots lanes owning one (virtual) row.
+struct Lanes {
+  int gw, lig, slot, lane, c0;
+};
+
+template <int LANES, int VEC>
+__device__ __forceinline__ Lanes lanes_of(int slots) {
+  Lanes L;
+  L.gw = LANES * slots;
+  L.lig = threadIdx.x & (L.gw - 1);
+  L.slot = L.lig / LANES;
+  L.lane = L.lig & (LANES - 1);
+  L.c0 = (blockIdx.y * LANES + L.lane) * VEC;
+  return L;
+}
+
+// sum_{e in [beg, end)} w_e M[col[e], c0 .. c0+VEC), every slice of the group holding the total
+template <int LANES, int VEC, bool USE_VAL>
+__device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, int64_t beg, int64_t end,
+                                                           const Lanes& L, int slots, bool cok) {
   using V = Vec<VEC>;
   constexpr int UNR = LANES >= 4 ? 8 : 4;
-  const int gw = LANES * slots;
-  const int lig = threadIdx.x & (gw - 1);
-  const int slot = lig / LANES;
-  const int lane = lig & (LANES - 1);
-  const int64_t row = (int64_t)blockIdx.x * (kBlock / gw) + threadIdx.x / gw;
-  const bool live = row < p.n;
-  const int c0 = (blockIdx.y * LANES + lane) * VEC;
-  const bool cok = live && c0 < p.w;
-
-  int64_t beg = 0, end = 0;
-  if (live) {
-    beg = p.row_ptr[row];
-    end = p.row_ptr[row + 1];
-  }
   typename V::T acc = V::zero();
-  const float* Mc = p.M + c0;
-  for (int64_t base = beg; base < end; base += gw) {
-    const int cnt = (int)((end - base) < gw ? (end - base) : gw);
+  const float* Mc = p.M + L.c0;
+  for (int64_t base = beg; base < end; base += L.gw) {
+    const int cnt = (int)((end - base) < L.gw ? (end - base) : L.gw);
     int my_j = 0;
     float my_w = 0.f;
-    if (lig < cnt) {
-      my_j = p.col[base + lig];
-      my_w = USE_VAL ? p.val[base + lig] : p.dinv[my_j];
+    if (L.lig < cnt) {
+      my_j = p.col[base + L.lig];
+      my_w = USE_VAL ? p.val[base + L.lig] : p.dinv[my_j];
     }
     for (int t = 0; t < cnt; t += slots * UNR) {
       int jj[UNR];
@@ -108,11 +124,11 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
       typename V::T xs[UNR];
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
-        const int e = t + u * slots + slot;
+        const int e = t + u * slots + L.slot;
         ok[u] = e < cnt;
         const int src = ok[u] ? e : 0;
-        jj[u] = __shfl(my_j, src, gw);
-        ww[u] = __shfl(my_w, src, gw);
+        jj[u] = __shfl(my_j, src, L.gw);
+        ww[u] = __shfl(my_w, src, L.gw);
       }
 #pragma unroll
       for (int u = 0; u < UNR; ++u) xs[u] = (ok[u] && cok) ? V::load(Mc + (int64_t)jj[u] * p.ldm) : V::zero();
@@ -120,10 +136,16 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
       for (int u = 0; u < UNR; ++u) V::fma(acc, ok[u] ? ww[u] : 0.f, xs[u]);
     }
   }
-  // sum the slices: after this every slice holds the full row
-  for (int o = LANES; o < gw; o <<= 1) V::add_xor(acc, o, gw);
-  if (!live) return;
+  for (int o = LANES; o < L.gw; o <<= 1) V::add_xor(acc, o, L.gw);
+  return acc;
+}
 
+// Scale, bias and epilogue of one row; slice 0 writes.
+template <int LANES, int VEC, int EPI, bool USE_VAL>
+__device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, const typename Vec<VEC>::T& acc,
+                                           const Lanes& L, bool cok) {
+  using V = Vec<VEC>;
+  const int c0 = L.c0;
   const float s = USE_VAL ? 1.f : p.dinv[row];
   float z[VEC];
 #pragma unroll
@@ -132,7 +154,6 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
     z[i] = s * V::get(acc, i);
     if (p.bias && c < p.w) z[i] += p.bias[c];
   }
-
   if constexpr (EPI == AGG_SOFTMAX) {
     // whole logits row is held by each slice (w <= LANES * VEC); slice 0 writes
     float mx = -INFINITY;
@@ -154,8 +175,8 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
     for (int i = 0; i < VEC; ++i)
       if (c0 + i == y) zy = z[i];
     zy = group_sum<LANES>(zy);
-    if (slot != 0) return;
-    if (lane == 0) p.row_loss[row] = (logf(se) + mx) - zy;
+    if (L.slot != 0) return;
+    if (L.lane == 0) p.row_loss[row] = (logf(se) + mx) - zy;
     if (!cok) return;
     const float inv_se = 1.f / se;
     float gv[VEC];
@@ -176,9 +197,8 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
       for (int i = 0; i < VEC; ++i)
         if (c0 + i < p.w) lg[i] = z[i];
     }
-    return;
   } else {
-    if (!cok || slot != 0) return;
+    if (!cok || L.slot != 0) return;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
       if constexpr (EPI == AGG_RELU) z[i] = fmaxf(z[i], 0.f);
@@ -199,40 +219,116 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots) {
   }
 }
 
-template <int LANES, int VEC, int EPI>
-gcn_status launch3(const AggParams& p, int slots, hipStream_t s) {
-  const int gw = LANES * slots;
-  dim3 grid((unsigned)ceil_div(p.n, kBlock / gw), (unsigned)ceil_div(p.w, LANES * VEC));
-  if constexpr (EPI == AGG_NONE) {
-    if (p.val) {
-      hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, true>), grid, dim3(kBlock), 0, s, p, slots);
-      return check_launch("spmm");
-    }
+// Every row whose length is at most skip_over (all rows when there is no split plan).
+template <int LANES, int VEC, int EPI, bool USE_VAL>
+__global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, int64_t skip_over) {
+  const Lanes L = lanes_of<LANES, VEC>(slots);
+  const int64_t row = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
+  if (row >= p.n) return;  // whole groups leave together
+  const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
+  if (end - beg > skip_over) return;
+  const bool cok = L.c0 < p.w;
+  const auto acc = accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok);
+  finish_row<LANES, VEC, EPI, USE_VAL>(p, row, acc, L, cok);
+}
+
+// One group per chunk of a long row: partial[ch, :] = sum over the chunk's entries.
+template <int LANES, int VEC, bool USE_VAL>
+__global__ void __launch_bounds__(kBlock) k_chunks(AggParams p, gcn_split sp, int slots, float* part, int64_t pw) {
+  const Lanes L = lanes_of<LANES, VEC>(slots);
+  const int64_t gi = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
+  if (gi >= sp.n_chunk) return;
+  const int64_t ch = sp.order ? sp.order[gi] : gi;
+  const int32_t h = sp.owner[ch];
+  const int64_t row = sp.rows[h];
+  const int64_t beg = p.row_ptr[row] + (ch - sp.first[h]) * (int64_t)GCN_SPLIT_CHUNK;
+  const int64_t rend = p.row_ptr[row + 1];
+  const int64_t end = beg + GCN_SPLIT_CHUNK < rend ? beg + GCN_SPLIT_CHUNK : rend;
+  const bool cok = L.c0 < p.w;
+  const auto acc = accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok);
+  if (cok && L.slot == 0) Vec<VEC>::store(part + ch * pw + L.c0, acc);
+}
+
+// One group per long row: add its chunk sums in chunk order, then the row epilogue.
+template <int LANES, int VEC, int EPI, bool USE_VAL>
+__global__ void __launch_bounds__(kBlock) k_combine(AggParams p, gcn_split sp, int slots, const float* part,
+                                                    int64_t pw) {
+  using V = Vec<VEC>;
+  const Lanes L = lanes_of<LANES, VEC>(slots);
+  const int64_t h = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
+  if (h >= sp.n_long) return;
+  const bool cok = L.c0 < p.w;
+  typename V::T acc = V::zero();
+  if (cok)
+    for (int64_t ch = sp.first[h]; ch < sp.first[h + 1]; ++ch) V::add(acc, V::load(part + ch * pw + L.c0));
+  finish_row<LANES, VEC, EPI, USE_VAL>(p, sp.rows[h], acc, L, cok);
+}
+
+struct Launch {
+  const AggParams* p;
+  const gcn_split* sp;
+  float* part;
+  int64_t pw;
+  int slots, chunk_slots;
+  hipStream_t s;
+};
+
+template <int LANES, int VEC, int EPI, bool USE_VAL>
+gcn_status launch4(const Launch& a) {
+  const AggParams& p = *a.p;
+  const bool split = has_split(a.sp);
+  const int64_t skip = split ? (int64_t)GCN_SPLIT_MIN : INT64_MAX;
+  const unsigned gy = (unsigned)ceil_div(p.w, LANES * VEC);
+  {
+    const int gw = LANES * a.slots;
+    dim3 grid((unsigned)ceil_div(p.n, kBlock / gw), gy);
+    hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, a.slots, skip);
+    GCN_TRY(check_launch("aggregate"));
   }
-  hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, false>), grid, dim3(kBlock), 0, s, p, slots);
-  return check_launch("aggregate");
+  if (!split) return GCN_OK;
+  {
+    const int gw = LANES * a.chunk_slots;
+    dim3 grid((unsigned)ceil_div(a.sp->n_chunk, kBlock / gw), gy);
+    hipLaunchKernelGGL((k_chunks<LANES, VEC, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, *a.sp, a.chunk_slots,
+                       a.part, a.pw);
+    GCN_TRY(check_launch("aggregate chunks"));
+  }
+  {
+    dim3 grid((unsigned)ceil_div(a.sp->n_long, kBlock / LANES), gy);
+    hipLaunchKernelGGL((k_combine<LANES, VEC, EPI, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, *a.sp, 1, a.part,
+                       a.pw);
+    return check_launch("aggregate combine");
+  }
+}
+
+template <int LANES, int VEC, int EPI>
+gcn_status launch3(const Launch& a) {
+  if constexpr (EPI == AGG_NONE) {
+    if (a.p->val) return launch4<LANES, VEC, EPI, true>(a);
+  }
+  return launch4<LANES, VEC, EPI, false>(a);
 }
 
 template <int LANES, int VEC>
-gcn_status launch2(const AggParams& p, int slots, hipStream_t s) {
-  switch (p.epi) {
-    case AGG_NONE: return launch3<LANES, VEC, AGG_NONE>(p, slots, s);
-    case AGG_RELU: return launch3<LANES, VEC, AGG_RELU>(p, slots, s);
-    case AGG_MASK: return launch3<LANES, VEC, AGG_MASK>(p, slots, s);
-    default: return launch3<LANES, VEC, AGG_SOFTMAX>(p, slots, s);
+gcn_status launch2(const Launch& a) {
+  switch (a.p->epi) {
+    case AGG_NONE: return launch3<LANES, VEC, AGG_NONE>(a);
+    case AGG_RELU: return launch3<LANES, VEC, AGG_RELU>(a);
+    case AGG_MASK: return launch3<LANES, VEC, AGG_MASK>(a);
+    default: return launch3<LANES, VEC, AGG_SOFTMAX>(a);
   }
 }
 
 template <int VEC>
-gcn_status launch1(const AggParams& p, int lanes, int slots, hipStream_t s) {
+gcn_status launch1(const Launch& a, int lanes) {
   switch (lanes) {
-    case 1: return launch2<1, VEC>(p, slots, s);
-    case 2: return launch2<2, VEC>(p, slots, s);
-    case 4: return launch2<4, VEC>(p, slots, s);
-    case 8: return launch2<8, VEC>(p, slots, s);
-    case 16: return launch2<16, VEC>(p, slots, s);
-    case 32: return launch2<32, VEC>(p, slots, s);
-    default: return launch2<64, VEC>(p, slots, s);
+    case 1: return launch2<1, VEC>(a);
+    case 2: return launch2<2, VEC>(a);
+    case 4: return launch2<4, VEC>(a);
+    case 8: return launch2<8, VEC>(a);
+    case 16: return launch2<16, VEC>(a);
+    case 32: return launch2<32, VEC>(a);
+    default: return launch2<64, VEC>(a);
   }
 }
 
@@ -252,23 +348,41 @@ int pick_slots(int lanes, int64_t nnz, int64_t rows) {
   return s;
 }
 
+bool use_vec4(const AggParams& p) {
+  return p.ldm % 4 == 0 && p.ldz % 4 == 0 && aligned16(p.M) && aligned16(p.Z) &&
+         (p.epi != AGG_MASK || (p.ldmask % 4 == 0 && aligned16(p.mask)));
+}
+
 }  // namespace
 
-gcn_status launch_aggregate(const AggParams& p, int64_t nnz, hipStream_t s) {
+size_t aggregate_workspace(const gcn_split* split, int32_t w) {
+  if (!has_split(split)) return 0;
+  return sizeof(float) * (size_t)split->n_chunk * (size_t)round_up(w, 4);
+}
+
+gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* split, void* ws,
+                            hipStream_t s) {
   if (p.n == 0 || p.w == 0) return GCN_OK;
-  const bool vec4 = p.ldm % 4 == 0 && p.ldz % 4 == 0 && aligned16(p.M) && aligned16(p.Z) &&
-                    (p.epi != AGG_MASK || (p.ldmask % 4 == 0 && aligned16(p.mask)));
+  const bool vec4 = use_vec4(p);
   const int vec = vec4 ? 4 : 1;
   int need = (int)ceil_div(p.w, vec);
   int lanes = 1;
   while (lanes < need && lanes < 64) lanes <<= 1;
   if (p.epi == AGG_SOFTMAX && need > lanes)
     return fail(GCN_E_UNSUPPORTED, "softmax epilogue needs width <= 256 (vector) or 64 (scalar)");
-  const int slots = pick_slots(lanes, nnz, p.n);
+  if (has_split(split) && !ws) return fail(GCN_E_INVALID, "aggregation of split rows needs a workspace");
+  Launch a;
+  a.p = &p;
+  a.sp = split;
+  a.part = static_cast<float*>(ws);
+  a.pw = round_up(p.w, 4);
+  a.slots = pick_slots(lanes, nnz, p.n);
+  a.chunk_slots = std::min(64 / lanes, 16);
+  a.s = s;
   char name[64];
   snprintf(name, sizeof name, "%s_w%d", p.val ? "spmm" : "aggregate", p.w);
   ProfScope prof(name, p.w, p.n, nnz, s);
-  return vec4 ? launch1<4>(p, lanes, slots, s) : launch1<1>(p, lanes, slots, s);
+  return vec4 ? launch1<4>(a, lanes) : launch1<1>(a, lanes);
 }
 
 }  // namespace gcn

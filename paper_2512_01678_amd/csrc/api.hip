@@ -46,6 +46,8 @@ gcn_status check_graph(const gcn_graph* g, const char* who) {
   if (g->n < 0) return fail(GCN_E_INVALID, std::string(who) + ": negative node count");
   if (g->n > 0 && (!g->row_ptr || !g->col_idx || !g->dinv))
     return fail(GCN_E_INVALID, std::string(who) + ": graph arrays missing");
+  if (g->split.rows && g->split.n_long > 0 && (!g->split.first || !g->split.owner))
+    return fail(GCN_E_INVALID, std::string(who) + ": split plan arrays missing");
   return GCN_OK;
 }
 
@@ -129,9 +131,10 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   const bool run = a.base != nullptr;
   if (order == GCN_AGGREGATE_FIRST) {
     // P = A_hat H_in (kept for the backward pass), then H_out = act(P W + b)
+    void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_in));
     if (run) {
       AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in);
-      GCN_TRY(launch_aggregate(p, g->nnz, s));
+      GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
       GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
       q.bias = b;
       q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
@@ -144,6 +147,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   float* M = a.take<float>((int64_t)n * ldm);
   float* row_loss = L->act == GCN_ACT_SOFTMAX_CE ? a.take<float>(n) : nullptr;
   void* cws = L->act == GCN_ACT_SOFTMAX_CE ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+  void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_out));
   if (!run) return GCN_OK;
   if (x) {
     AggParams p{};
@@ -157,7 +161,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.Z = M;
     p.ldz = ldm;
     p.epi = AGG_NONE;
-    GCN_TRY(launch_aggregate(p, x->nnz, s));
+    GCN_TRY(launch_aggregate(p, x->nnz, nullptr, nullptr, s));
   } else {
     GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
     GCN_TRY(launch_gemm(q, nullptr, s));
@@ -173,7 +177,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.ldl = L->ld_out;
     p.inv_n = n > 0 ? 1.f / (float)n : 0.f;
   }
-  GCN_TRY(launch_aggregate(p, g->nnz, s));
+  GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
   if (L->act == GCN_ACT_SOFTMAX_CE)
     GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
   return GCN_OK;
@@ -192,6 +196,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     void* gws = a.take<char>((int64_t)gemm_workspace(dw));
     const int64_t ldt = pitch4(L->f_in);
     float* T = Gprev ? a.take<float>((int64_t)n * ldt) : nullptr;
+    void* aws = Gprev ? a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_in)) : nullptr;
     if (!run) return GCN_OK;
     GCN_TRY(launch_gemm(dw, gws, s));
     GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
@@ -202,7 +207,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
       p.epi = AGG_MASK;
       p.mask = Hin;
       p.ldmask = L->ld_in;
-      GCN_TRY(launch_aggregate(p, g->nnz, s));
+      GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
     }
     return GCN_OK;
   }
@@ -211,8 +216,11 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   float* Q = a.take<float>((int64_t)n * ldq);
   GemmParams dw = gemm(L->f_in, L->f_out, n, Hin, L->ld_in, true, Q, ldq, false, dW, L->f_out);
   void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(dw));
+  const size_t agg_need = std::max(aggregate_workspace(&g->split, L->f_out),
+                                   x ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
+  void* aws = a.take<char>((int64_t)agg_need);
   if (!run) return GCN_OK;
-  GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq), g->nnz, s));
+  GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq), g->nnz, &g->split, aws, s));
   if (x) {
     AggParams p{};
     p.n = x->f;
@@ -225,7 +233,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     p.Z = dW;
     p.ldz = L->f_out;
     p.epi = AGG_NONE;
-    GCN_TRY(launch_aggregate(p, x->nnz, s));
+    GCN_TRY(launch_aggregate(p, x->nnz, &x->csc_split, aws, s));
   } else {
     GCN_TRY(launch_gemm(dw, gws, s));
   }
@@ -322,6 +330,8 @@ gcn_status gcn_build_csr(int32_t n, int64_t n_edges, const int32_t* d_src, const
   if (n_edges > 0 && (!d_src || !d_dst)) return fail(GCN_E_INVALID, "gcn_build_csr: edge arrays missing");
   if (!g->row_ptr || (n > 0 && (!g->deg || !g->dinv || !g->col_idx)))
     return fail(GCN_E_INVALID, "gcn_build_csr: output arrays missing");
+  if (g->split.rows && (!g->split.first || !g->split.owner || g->split.cap < 0))
+    return fail(GCN_E_INVALID, "gcn_build_csr: split plan arrays missing");
   if (g->nnz_cap < 0) return fail(GCN_E_INVALID, "gcn_build_csr: negative capacity");
   g->n = n;
   return run_build_csr(n, n_edges, d_src, d_dst, g, d_ws, stream);
@@ -342,6 +352,8 @@ gcn_status gcn_feature_stats(const float* d_X, int32_t n, int32_t f, int64_t ldx
   if (!info || (n > 0 && f > 0 && !d_X)) return fail(GCN_E_INVALID, "gcn_feature_stats: X and info are required");
   if (x && (!x->row_ptr || !x->col || !x->val || (csc && (!x->row || !x->cval))))
     return fail(GCN_E_INVALID, "gcn_feature_stats: sparse output arrays missing");
+  if (x && csc && x->csc_split.rows && (!x->csc_split.first || !x->csc_split.owner || x->csc_split.cap < 0))
+    return fail(GCN_E_INVALID, "gcn_feature_stats: split plan arrays missing");
   return run_feature_stats(d_X, n, f, ldx, tau_num, tau_den, force_mode, d_row_nnz, info, x, d_ws, stream);
 }
 
@@ -447,20 +459,23 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
 }
 
 gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm, const float* d_bias,
-                         int32_t epi, const float* d_mask, int64_t ldmask, float* d_Z, int64_t ldz,
-                         hipStream_t stream) {
+                         int32_t epi, const float* d_mask, int64_t ldmask, float* d_Z, int64_t ldz, void* d_ws,
+                         size_t* ws_bytes, hipStream_t stream) {
   g_err.clear();
   GCN_TRY(check_graph(g, "gcn_aggregate"));
   if (w < 0 || ldm < w || ldz < w) return fail(GCN_E_INVALID, "gcn_aggregate: bad width or pitch");
   if (epi < GCN_EPI_NONE || epi > GCN_EPI_MASK) return fail(GCN_E_INVALID, "gcn_aggregate: unknown epilogue");
   if (epi == GCN_EPI_MASK && (!d_mask || ldmask < w)) return fail(GCN_E_INVALID, "gcn_aggregate: mask missing");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, aggregate_workspace(&g->split, w), "gcn_aggregate", &query));
+  if (query) return GCN_OK;
   if (g->n > 0 && w > 0 && (!d_M || !d_Z)) return fail(GCN_E_INVALID, "gcn_aggregate: d_M and d_Z are required");
   AggParams p = graph_agg(g, w, d_M, ldm, d_Z, ldz);
   p.bias = d_bias;
   p.epi = epi == GCN_EPI_RELU ? AGG_RELU : (epi == GCN_EPI_MASK ? AGG_MASK : AGG_NONE);
   p.mask = d_mask;
   p.ldmask = ldmask;
-  return launch_aggregate(p, g->nnz, stream);
+  return launch_aggregate(p, g->nnz, &g->split, d_ws, stream);
 }
 
 gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_A, int64_t lda,
@@ -489,10 +504,15 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
 
 gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, const float* d_val,
                     int64_t b_rows, int32_t w, const float* d_B, int64_t ldb, float* d_C, int64_t ldc,
-                    hipStream_t stream) {
+                    const gcn_split* split, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
   g_err.clear();
   if (nrows < 0 || nrows > INT32_MAX || w < 0 || b_rows < 0 || ldb < w || ldc < w)
     return fail(GCN_E_INVALID, "gcn_spmm: bad size or pitch");
+  if (split && split->rows && split->n_long > 0 && (!split->first || !split->owner))
+    return fail(GCN_E_INVALID, "gcn_spmm: split plan arrays missing");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, aggregate_workspace(split, w), "gcn_spmm", &query));
+  if (query) return GCN_OK;
   if (nrows > 0 && w > 0 && (!d_ptr || !d_idx || !d_val || !d_B || !d_C))
     return fail(GCN_E_INVALID, "gcn_spmm: NULL argument");
   AggParams p{};
@@ -506,7 +526,7 @@ gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, c
   p.Z = d_C;
   p.ldz = ldc;
   p.epi = AGG_NONE;
-  return launch_aggregate(p, -1, stream);
+  return launch_aggregate(p, -1, split, d_ws, stream);
 }
 
 gcn_status gcn_column_sums(int64_t rows, int32_t w, const float* d_G, int64_t ldg, float* d_out,

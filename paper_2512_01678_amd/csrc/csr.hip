@@ -35,6 +35,7 @@ struct CsrWs {
   void* scan;
   uint32_t* bitmap;   // kLargeBlocks * words
   int64_t words;
+  void* split;        // hub split plan scratch
 };
 
 CsrWs carve(Arena& a, int32_t n, int64_t n_edges) {
@@ -48,6 +49,7 @@ CsrWs carve(Arena& a, int32_t n, int64_t n_edges) {
   w.scan = a.take<char>((int64_t)scan_workspace((int64_t)n + 1));
   w.words = ceil_div(n, 32);
   w.bitmap = a.take<uint32_t>(kLargeBlocks * w.words);
+  w.split = a.take<char>((int64_t)split_workspace(n));
   return w;
 }
 
@@ -328,6 +330,8 @@ gcn_status run_build_csr(int32_t n, int64_t n_edges, const int32_t* src, const i
                        g->row_ptr, g->deg, g->col_idx, g->dinv);
     GCN_TRY(check_launch("csr compact"));
   }
+  g->split.order = nullptr;
+  if (g->split.rows) GCN_TRY(build_split(g->row_ptr, n, &g->split, false, w.split, s));
   GCN_HIP(hipStreamSynchronize(s), "csr sync");
   return GCN_OK;
 }

@@ -28,6 +28,7 @@ struct FeatWs {
   int32_t* chunk_off;  // nchunks * f
   int32_t* col_tot;    // f
   int64_t nchunks;
+  void* split;         // split plan scratch for long CSC columns
 };
 
 FeatWs carve(Arena& a, int32_t n, int32_t f, bool csc) {
@@ -39,6 +40,7 @@ FeatWs carve(Arena& a, int32_t n, int32_t f, bool csc) {
   w.chunk_cnt = a.take<int32_t>(csc ? w.nchunks * f : 0);
   w.chunk_off = a.take<int32_t>(csc ? w.nchunks * f : 0);
   w.col_tot = a.take<int32_t>(csc ? f : 0);
+  w.split = a.take<char>(csc ? (int64_t)split_workspace(f) : 0);
   return w;
 }
 
@@ -180,6 +182,7 @@ gcn_status run_feature_stats(const float* X, int32_t n, int32_t f, int64_t ldx, 
                          w.chunk_off, x->row, x->cval);
       GCN_TRY(check_launch("dense to csc"));
     }
+    if (x->csc_split.rows) GCN_TRY(build_split(x->col_ptr, f, &x->csc_split, true, w.split, s));
   }
   GCN_HIP(hipStreamSynchronize(s), "feature sync");
   return GCN_OK;

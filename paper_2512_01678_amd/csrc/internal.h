@@ -90,7 +90,17 @@ struct AggParams {
   int64_t ldl;
   float inv_n;             // 1 / n
 };
-gcn_status launch_aggregate(const AggParams& p, int64_t nnz, hipStream_t s);
+// Z over all rows; rows longer than GCN_SPLIT_MIN go through the split plan when one
+// is given (its chunk sums live in ws, aggregate_workspace() bytes).
+size_t aggregate_workspace(const gcn_split* split, int32_t w);
+gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* split, void* ws,
+                            hipStream_t s);
+inline bool has_split(const gcn_split* sp) { return sp && sp->rows && sp->n_long > 0; }
+
+// split plan of the long rows of a compressed matrix with offsets ptr[0..nrows]
+size_t split_workspace(int64_t nrows);
+gcn_status build_split(const int64_t* ptr, int64_t nrows, gcn_split* sp, bool chunk_major, void* ws,
+                       hipStream_t s);
 
 enum GemmEpi { GEMM_NONE = 0, GEMM_RELU = 1, GEMM_MASK = 2 };
 // C(m,n) = sum_k A(m,k) B(k,n) with A(m,k) = A[m*lda+k] (ta=false) or A[k*lda+m] (ta=true),

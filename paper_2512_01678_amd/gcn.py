@@ -39,14 +39,22 @@ class GcnError(RuntimeError):
         super().__init__(f"{where}: {name}: {msg}")
 
 
+SPLIT_MIN, SPLIT_CHUNK = 4096, 2048
+
+
+class gcn_split(C.Structure):
+    _fields_ = [("n_long", i32), ("n_chunk", i64), ("cap", i64), ("rows", P), ("first", P), ("owner", P),
+                ("order", P)]
+
+
 class gcn_graph(C.Structure):
     _fields_ = [("n", i32), ("nnz", i64), ("nnz_cap", i64), ("row_ptr", P), ("col_idx", P),
-                ("deg", P), ("dinv", P)]
+                ("deg", P), ("dinv", P), ("split", gcn_split)]
 
 
 class gcn_sparse_x(C.Structure):
     _fields_ = [("n", i32), ("f", i32), ("nnz", i64), ("row_ptr", P), ("col", P), ("val", P),
-                ("col_ptr", P), ("row", P), ("cval", P)]
+                ("col_ptr", P), ("row", P), ("cval", P), ("csc_split", gcn_split)]
 
 
 class gcn_feature_info(C.Structure):
@@ -87,9 +95,9 @@ _SIG = {
                             P, P, P, P, P, P, C.POINTER(sz), P]),
     "gcn_epoch": (i32, [C.POINTER(gcn_model), C.POINTER(gcn_graph), P, C.POINTER(gcn_sparse_x), P, P,
                         P, C.POINTER(sz), P]),
-    "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i32, P, i64, P, i64, P]),
+    "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i32, P, i64, P, i64, P, C.POINTER(sz), P]),
     "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
-    "gcn_spmm": (i32, [i64, P, P, P, i64, i32, P, i64, P, i64, P]),
+    "gcn_spmm": (i32, [i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
     "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
     "gcn_profile_enable": (i32, [i32]),
@@ -160,17 +168,35 @@ def _run_ws(fn, args_before, args_after, where, ws: _Workspace | None, device):
 # ---------------------------------------------------------------------------
 
 
-class DeviceGraph:
-    """A + I in CSR on the device (owning torch tensors)."""
+class SplitPlan:
+    """Device buffers of a row-split plan (see gcn_split in gcn.h)."""
 
-    def __init__(self, n, row_ptr, col_idx, deg, dinv, nnz):
+    def __init__(self, entries: int, dev, order: bool):
+        cap = (3 * entries) // (2 * SPLIT_CHUNK) + 1  # bound on chunks (see gcn_split)
+        self.rows = torch.empty(cap, dtype=torch.int32, device=dev)
+        self.first = torch.empty(cap + 1, dtype=torch.int64, device=dev)
+        self.owner = torch.empty(cap, dtype=torch.int32, device=dev)
+        self.order = torch.empty(cap, dtype=torch.int64, device=dev) if order else None
+        self.c = gcn_split(0, 0, cap, _ptr(self.rows), _ptr(self.first), _ptr(self.owner), _ptr(self.order))
+
+
+class DeviceGraph:
+    """A + I in CSR on the device (owning torch tensors), with its hub split plan."""
+
+    def __init__(self, n, row_ptr, col_idx, deg, dinv, nnz, plan: SplitPlan | None, split_c):
         self.n = n
         self.row_ptr, self.col_idx, self.deg, self.dinv = row_ptr, col_idx, deg, dinv
         self.nnz = nnz
-        self.c = gcn_graph(n, nnz, col_idx.numel(), _ptr(row_ptr), _ptr(col_idx), _ptr(deg), _ptr(dinv))
+        self.plan = plan
+        self.c = gcn_graph(n, nnz, col_idx.numel(), _ptr(row_ptr), _ptr(col_idx), _ptr(deg), _ptr(dinv),
+                           split_c)
+
+    @property
+    def n_long(self):
+        return self.c.split.n_long
 
 
-def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None) -> DeviceGraph:
+def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None, split: bool = True) -> DeviceGraph:
     """gcn_build_csr on device int32 edge arrays; returns the graph (blocking)."""
     dev = src.device
     ne = src.numel()
@@ -178,16 +204,18 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None) -> Devi
     col = torch.empty(max(2 * ne + n, 1), dtype=torch.int32, device=dev)
     deg = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
     dinv = torch.empty(max(n, 1), dtype=torch.float32, device=dev)
-    g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv))
+    plan = SplitPlan(2 * ne + n, dev, order=False) if split else None
+    g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv),
+                  plan.c if plan else gcn_split())
     _run_ws(_lib.gcn_build_csr, (n, ne, _ptr(src), _ptr(dst), C.byref(g)), (P(_stream(stream)),),
             "gcn_build_csr", None, dev)
-    return DeviceGraph(n, row_ptr, col, deg, dinv, g.nnz)
+    return DeviceGraph(n, row_ptr, col, deg, dinv, g.nnz, plan, g.split)
 
 
 class SparseFeatures:
-    """X_csr (+ X_csc) on the device (owning torch tensors)."""
+    """X_csr (+ X_csc with its long-column split plan) on the device (owning torch tensors)."""
 
-    def __init__(self, n, f, nnz, dev, csc=True):
+    def __init__(self, n, f, nnz, dev, csc=True, split=True):
         cap = max(nnz, 1)
         self.row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
         self.col = torch.empty(cap, dtype=torch.int32, device=dev)
@@ -195,8 +223,10 @@ class SparseFeatures:
         self.col_ptr = torch.empty(f + 1, dtype=torch.int64, device=dev) if csc else None
         self.row = torch.empty(cap, dtype=torch.int32, device=dev) if csc else None
         self.cval = torch.empty(cap, dtype=torch.float32, device=dev) if csc else None
+        self.plan = SplitPlan(cap, dev, order=True) if (csc and split) else None
         self.c = gcn_sparse_x(n, f, nnz, _ptr(self.row_ptr), _ptr(self.col), _ptr(self.val),
-                              _ptr(self.col_ptr), _ptr(self.row), _ptr(self.cval))
+                              _ptr(self.col_ptr), _ptr(self.row), _ptr(self.cval),
+                              self.plan.c if self.plan else gcn_split())
 
     @property
     def nnz(self):
@@ -232,11 +262,11 @@ def feature_stats(X: torch.Tensor, tau=(4, 5), force_mode=-1, materialize=None, 
 
 
 def aggregate(g: DeviceGraph, M: torch.Tensor, out: torch.Tensor, bias=None, epi=EPI_NONE, mask=None,
-              stream=None):
+              ws: _Workspace | None = None, stream=None):
     w = M.shape[1]
-    _check(_lib.gcn_aggregate(C.byref(g.c), w, _ptr(M), _ld(M), _ptr(bias), epi, _ptr(mask),
-                              _ld(mask) if mask is not None else 0, _ptr(out), _ld(out),
-                              P(_stream(stream))), "gcn_aggregate")
+    _run_ws(_lib.gcn_aggregate, (C.byref(g.c), w, _ptr(M), _ld(M), _ptr(bias), epi, _ptr(mask),
+                                 _ld(mask) if mask is not None else 0, _ptr(out), _ld(out)),
+            (P(_stream(stream)),), "gcn_aggregate", ws, out.device)
     return out
 
 
@@ -256,10 +286,11 @@ def gemm(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, ws: _Workspace | Non
     return out
 
 
-def spmm(ptr, idx, val, B, out, stream=None):
+def spmm(ptr, idx, val, B, out, split: gcn_split | None = None, stream=None):
     nrows = ptr.numel() - 1
-    _check(_lib.gcn_spmm(nrows, _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B),
-                         _ld(B), _ptr(out), _ld(out), P(_stream(stream))), "gcn_spmm")
+    _run_ws(_lib.gcn_spmm, (nrows, _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B), _ld(B),
+                            _ptr(out), _ld(out), C.byref(split) if split is not None else None),
+            (P(_stream(stream)),), "gcn_spmm", None, out.device)
     return out
 
 

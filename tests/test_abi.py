@@ -42,7 +42,7 @@ def test_struct_layout_matches_c(G, tmp_path):
     structs = {
         "gcn_graph": G.gcn_graph, "gcn_sparse_x": G.gcn_sparse_x, "gcn_feature_info": G.gcn_feature_info,
         "gcn_layer": G.gcn_layer, "gcn_model": G.gcn_model, "gcn_adam_tensor": G.gcn_adam_tensor,
-        "gcn_profile_record": G.gcn_profile_record,
+        "gcn_profile_record": G.gcn_profile_record, "gcn_split": G.gcn_split,
     }
     lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "gcn.h"', "int main(void) {"]
     for sname, cls in structs.items():
@@ -100,10 +100,20 @@ def test_host_validation_rejects_bad_calls(G):
     nb2 = G.sz(1 << 20)
     assert L.gcn_gemm(G.OP_NN, 4, 4, 4, None, 4, 1, 4, 1, 4, None, 0, None, 0, 1, C.byref(nb2), None) == G.E_INVALID
     # aggregate: NULL graph, mask epilogue without mask
-    assert L.gcn_aggregate(None, 4, 1, 4, None, 0, None, 0, 1, 4, None) == G.E_INVALID
+    assert L.gcn_aggregate(None, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
     g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1)
-    assert L.gcn_aggregate(C.byref(g2), 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None) == G.E_INVALID
-    assert L.gcn_aggregate(C.byref(g2), 4, 1, 3, None, 0, None, 0, 1, 4, None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(g2), 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None, C.byref(nb),
+                           None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(g2), 4, 1, 3, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    # a split plan with long rows needs its chunk sums in the workspace
+    sp = G.gcn_split(3, 50, 64, 1, 1, 1, None)
+    g3 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, sp)
+    assert L.gcn_aggregate(C.byref(g3), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.OK
+    assert nb.value == 50 * 40 * 4
+    bad = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, G.gcn_split(3, 50, 64, 1, None, 1, None))
+    assert L.gcn_aggregate(C.byref(bad), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.E_INVALID
+    # spmm: bad pitch
+    assert L.gcn_spmm(10, 1, 1, 1, 5, 8, 1, 7, 1, 8, None, None, C.byref(nb), None) == G.E_INVALID
     # adam: step 0, too many tensors
     assert L.gcn_adam(None, 0, 0, 0.01, 0.9, 0.999, 1e-8, None) == G.E_INVALID
     arr = (G.gcn_adam_tensor * 17)()

@@ -310,3 +310,106 @@ def test_adam(G, orc):
         np.testing.assert_allclose(host(dm[i]), wm, rtol=2e-6, atol=1e-7)
         np.testing.assert_allclose(host(dv[i]), wv, rtol=2e-6, atol=1e-9)
         assert_mag_close(host(dp[i]), want, np.abs(ps[i]) + 0.01, f"adam tensor {i}", rtol=1e-5)
+
+
+# ---------------------------------------------------------------------------
+# hub rows split into chunks (rows longer than GCN_SPLIT_MIN entries)
+# ---------------------------------------------------------------------------
+
+
+def expected_plan(ptr, chunk, minlen):
+    lens = np.diff(ptr)
+    rows = np.nonzero(lens > minlen)[0]
+    nch = (lens[rows] + chunk - 1) // chunk
+    first = np.concatenate([[0], np.cumsum(nch)])
+    owner = np.repeat(np.arange(rows.size), nch)
+    return rows, first, owner
+
+
+@pytest.fixture(scope="module")
+def hub_graph(G, orc):
+    rng = np.random.default_rng(9)
+    n = 20000
+    s1, d1 = gs.chung_lu(n, 60000, seed=5)
+    hubs = [(3, 15000), (11, 5000), (12, 4000), (19999, 4200)]
+    ss, dd = [s1], [d1]
+    for h, k in hubs:
+        ss.append(np.full(k, h, np.int32))
+        dd.append(rng.choice(n, k, replace=False).astype(np.int32))
+    s = np.concatenate(ss)
+    d = np.concatenate(dd)
+    og = orc.build_csr(n, s, d)
+    dg = G.build_csr(n, dev(s), dev(d))
+    rows, first, owner = expected_plan(og.row_ptr, G.SPLIT_CHUNK, G.SPLIT_MIN)
+    assert dg.n_long == rows.size >= 3
+    assert dg.c.split.n_chunk == first[-1]
+    np.testing.assert_array_equal(host(dg.plan.rows)[:rows.size], rows)
+    np.testing.assert_array_equal(host(dg.plan.first)[:rows.size + 1], first)
+    np.testing.assert_array_equal(host(dg.plan.owner)[:first[-1]], owner)
+    return og, dg
+
+
+@pytest.mark.parametrize("w", [7, 40, 128, 256])
+def test_aggregate_split_hubs(G, orc, hub_graph, w):
+    og, dg = hub_graph
+    rng = np.random.default_rng(w + 1)
+    n = og.n
+    M = rng.standard_normal((n, w)).astype(np.float32)
+    b = rng.standard_normal(w).astype(np.float32)
+    mask = rng.standard_normal((n, w)).astype(np.float32)
+    ld = G.pitch(w)
+    Md = pitched(M, ld)
+    Zd = pitched(np.zeros((n, w), np.float32), ld)
+    Z, mag = orc.aggregate(og, M, b, want_mag=True)
+    for epi in (G.EPI_NONE, G.EPI_RELU, G.EPI_MASK):
+        G.aggregate(dg, Md, Zd, bias=dev(b), epi=epi, mask=pitched(mask, ld) if epi == G.EPI_MASK else None)
+        want = Z if epi == G.EPI_NONE else (np.maximum(Z, 0) if epi == G.EPI_RELU else Z * (mask > 0))
+        assert_mag_close(host(Zd), want, mag, f"split aggregate w={w} epi={epi}")
+    first = host(Zd).copy()
+    G.aggregate(dg, Md, Zd, bias=dev(b), epi=G.EPI_MASK, mask=pitched(mask, ld))
+    np.testing.assert_array_equal(host(Zd), first)
+
+
+def test_softmax_layer_on_split_hubs(G, orc, hub_graph):
+    og, dg = hub_graph
+    n = og.n
+    rng = np.random.default_rng(4)
+    H = np.maximum(rng.standard_normal((n, 64)), 0).astype(np.float32)
+    W = (rng.standard_normal((64, 41)) / 8).astype(np.float32)
+    b = (rng.standard_normal(41) * 0.1).astype(np.float32)
+    y = rng.integers(0, 41, n).astype(np.int32)
+    L = G.make_layer(64, 41, 64, G.pitch(41), G.ACT_SOFTMAX_CE, 1)
+    Hd = pitched(H, 64)
+    out = pitched(np.zeros((n, 41), np.float32), G.pitch(41))
+    logits = pitched(np.zeros((n, 41), np.float32), G.pitch(41))
+    loss = torch.zeros(1, device="cuda")
+    G.layer_fwd(dg, L, Hd, None, dev(W), dev(b), out, labels=dev(y), loss=loss, logits=logits)
+    Z = orc.aggregate(og, orc.matmul(H, W), b)
+    mag = orc.aggregate(og, orc.matmul(np.abs(H), np.abs(W)), np.abs(b))
+    assert_mag_close(host(logits), Z, mag, "split logits")
+    lo, Gr, _ = orc.softmax_ce(Z, y)
+    assert host(loss)[0] == pytest.approx(lo, rel=1e-4)
+    np.testing.assert_allclose(host(out), Gr, rtol=0, atol=1e-4 * np.abs(Gr).max())
+
+
+def test_sparse_backward_long_columns(G, orc):
+    """X with few, dense columns: every CSC column is long and goes through chunks
+    processed chunk-index-major."""
+    n, f, w = 30000, 48, 40
+    X = gs.features_bernoulli(n, f, 0.4, seed=2, binary=False)
+    rng = np.random.default_rng(1)
+    Q = rng.standard_normal((n, w)).astype(np.float32)
+    _, sx = G.feature_stats(dev(X), materialize=True)
+    cp, row, cval = orc.dense_to_csc(X)
+    rows, first, owner = expected_plan(cp, G.SPLIT_CHUNK, G.SPLIT_MIN)
+    sp = sx.c.csc_split
+    assert sp.n_long == rows.size == f and sp.n_chunk == first[-1]
+    np.testing.assert_array_equal(host(sx.plan.first)[:f + 1], first)
+    order = host(sx.plan.order)[:first[-1]]
+    np.testing.assert_array_equal(np.sort(order), np.arange(first[-1]))
+    k_of = order - first[owner[order]]
+    assert (np.diff(k_of) >= 0).all()          # chunk index never decreases along the order
+    dW = torch.empty((f, w), dtype=torch.float32, device="cuda")
+    G.spmm(sx.col_ptr, sx.row[:sx.nnz], sx.cval[:sx.nnz], dev(Q), dW, split=sp)
+    ref, mag = orc.spmm(cp, row, cval, Q, want_mag=True)
+    assert_mag_close(host(dW), ref, mag, "X_csc Q with long columns")

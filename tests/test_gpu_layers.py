@@ -275,3 +275,23 @@ def test_arxiv_like_full_size_sampled(G, orc):
             ref = (Q[rows] @ p.Ws[l].T.astype(np.float64)) * (Hs[l][rows] > 0)
             mag = aQ[rows] @ np.abs(p.Ws[l].T.astype(np.float64))
             assert_mag_close(host(m.grad[l - 1])[rows], ref, mag, f"full-size G_{l - 1} rows")
+
+
+def test_epoch_rmat_4096_features_sparse(G, orc):
+    """RMAT graph with 4096-wide nonnegative features at 10 % density (the RMAT workload's
+    recipe on 2^14 nodes): sparse path chosen by the probe, one epoch against the oracle."""
+    from gcn_synth import device
+    wl = gs.Workload("rmat14_p0.1", 1 << 14, "rmat", 1 << 18, (4096, 128, 32), "nonneg", 0.1, rmat_scale=14)
+    s, d = gs.rmat(14, 1 << 18)
+    n = wl.n
+    Xd = torch.zeros((n, 4096), device="cuda")
+    device.bernoulli_into(Xd, 0.1, seed=0, stream=3)
+    X = gs.features_bernoulli(n, 4096, 0.1, seed=0, stream=3, binary=False)
+    np.testing.assert_array_equal(host(Xd).astype(np.float32), X)
+    info, sx = G.feature_stats(Xd)
+    assert info["mode"] == G.SPARSE
+    p = Problem.__new__(Problem)
+    p.wl, p.og, p.dg = wl, orc.build_csr(n, s, d), G.build_csr(n, dev(s), dev(d))
+    p.X, p.y = X, gs.labels(n, 32)
+    p.Ws, p.bs = gs.make_weights(wl)
+    run_epochs(G, orc, p, 1, sparse=True)
