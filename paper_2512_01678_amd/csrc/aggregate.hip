@@ -380,7 +380,7 @@ gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* sp
   a.chunk_slots = std::min(64 / lanes, 16);
   a.s = s;
   char name[64];
-  snprintf(name, sizeof name, "%s_w%d", p.val ? "spmm" : "aggregate", p.w);
+  snprintf(name, sizeof name, "%s_w%d", p.tag ? p.tag : (p.val ? "spmm" : "aggregate"), p.w);
   ProfScope prof(name, p.w, p.n, nnz, s);
   return vec4 ? launch1<4>(a, lanes) : launch1<1>(a, lanes);
 }

@@ -161,6 +161,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.Z = M;
     p.ldz = ldm;
     p.epi = AGG_NONE;
+    p.tag = "spmm_xw";
     GCN_TRY(launch_aggregate(p, x->nnz, nullptr, nullptr, s));
   } else {
     GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
@@ -233,6 +234,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     p.Z = dW;
     p.ldz = L->f_out;
     p.epi = AGG_NONE;
+    p.tag = "spmm_xtq";
     GCN_TRY(launch_aggregate(p, x->nnz, &x->csc_split, aws, s));
   } else {
     GCN_TRY(launch_gemm(dw, gws, s));

@@ -89,6 +89,7 @@ struct AggParams {
   float* logits;           // optional copy of Z
   int64_t ldl;
   float inv_n;             // 1 / n
+  const char* tag;         // kernel family name for the profiler (NULL: derived)
 };
 // Z over all rows; rows longer than GCN_SPLIT_MIN go through the split plan when one
 // is given (its chunk sums live in ws, aggregate_workspace() bytes).
