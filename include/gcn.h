@@ -244,6 +244,7 @@ typedef struct gcn_model {
   float** grad;
   double lr, beta1, beta2, eps;  /* Adam hyperparameters (the paper: 0.01, 0.9, 0.999) */
   int32_t step;
+  int32_t* d_step;  /* optional device counter of completed steps; see gcn_epoch */
 } gcn_model;
 
 /*
@@ -252,7 +253,11 @@ typedef struct gcn_model {
  * one Adam step (bias-corrected, step t = m->step + 1) over every W and b.
  * Asynchronous; increments m->step on success.  Exactly one of d_X (dense,
  * pitch m->layers[0].ld_in) and x (sparse path) is non-NULL.  *d_loss receives
- * the mean loss of the forward pass.
+ * the mean loss of the forward pass.  When m->d_step is non-NULL the step number
+ * is read from and incremented in device memory instead (m->step is left alone),
+ * so the enqueued work depends on no host value that changes between epochs and
+ * one epoch can be captured in a HIP graph and replayed.  No call made by an
+ * epoch allocates, synchronises or records a memset.
  */
 gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const gcn_sparse_x* x,
                      const int32_t* d_labels, float* d_loss, void* d_ws, size_t* ws_bytes,
@@ -331,6 +336,11 @@ typedef struct gcn_adam_tensor {
  */
 gcn_status gcn_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, double lr, double beta1,
                     double beta2, double eps, hipStream_t stream);
+
+/* As gcn_adam, with the step read from *d_step (completed steps; this step is
+ * *d_step + 1) and *d_step incremented on the device afterwards. */
+gcn_status gcn_adam_device_step(const gcn_adam_tensor* t, int32_t count, int32_t* d_step, double lr,
+                                double beta1, double beta2, double eps, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing with HIP events (used by the benchmark).

@@ -21,10 +21,17 @@ struct AdamArgs {
   int64_t off[kMaxTensors + 1];
   int32_t count;
   float lr, b1, omb1, b2, omb2, eps, bc1, bc2;  // omb = 1 - b, formed in double
+  const int32_t* d_step;                        // when set: bc1, bc2 from 1 - b^(*d_step + 1)
+  double b1d, b2d;
 };
 
 __global__ void __launch_bounds__(256) k_adam(AdamArgs a) {
   const int64_t total = a.off[a.count];
+  if (a.d_step) {
+    const double t = (double)(*a.d_step + 1);
+    a.bc1 = (float)(1.0 - pow(a.b1d, t));
+    a.bc2 = (float)(1.0 - pow(a.b2d, t));
+  }
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
     int t = 0;
@@ -41,10 +48,14 @@ __global__ void __launch_bounds__(256) k_adam(AdamArgs a) {
   }
 }
 
+__global__ void k_step_increment(int32_t* d_step) {
+  if (threadIdx.x == 0) *d_step += 1;
+}
+
 }  // namespace
 
-gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, double lr, double b1,
-                       double b2, double eps, hipStream_t s) {
+gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, int32_t* d_step, double lr,
+                       double b1, double b2, double eps, hipStream_t s) {
   if (count > kMaxTensors) return fail(GCN_E_UNSUPPORTED, "gcn_adam: at most 16 tensors per call");
   AdamArgs a{};
   a.count = count;
@@ -64,11 +75,20 @@ gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, do
   a.eps = (float)eps;
   a.bc1 = (float)(1.0 - std::pow(b1, (double)step));
   a.bc2 = (float)(1.0 - std::pow(b2, (double)step));
+  a.d_step = d_step;
+  a.b1d = b1;
+  a.b2d = b2;
   const int64_t total = a.off[count];
-  if (total == 0) return GCN_OK;
-  const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 2048);
-  hipLaunchKernelGGL(k_adam, dim3(grid), dim3(256), 0, s, a);
-  return check_launch("adam");
+  if (total > 0) {
+    const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(total, 256), 2048);
+    hipLaunchKernelGGL(k_adam, dim3(grid), dim3(256), 0, s, a);
+    GCN_TRY(check_launch("adam"));
+  }
+  if (d_step) {
+    hipLaunchKernelGGL(k_step_increment, dim3(1), dim3(64), 0, s, d_step);
+    GCN_TRY(check_launch("adam step"));
+  }
+  return GCN_OK;
 }
 
 }  // namespace gcn

@@ -25,6 +25,10 @@
 // and applies the same epilogue.
 #include "internal.h"
 
+#ifndef GCN_AGG_UNR
+#define GCN_AGG_UNR 16  // neighbour-row loads kept in flight per lane, full-wavefront rows
+#endif
+
 namespace gcn {
 namespace {
 
@@ -101,22 +105,22 @@ __device__ __forceinline__ Lanes lanes_of(int slots) {
   return L;
 }
 
-// sum_{e in [beg, end)} w_e M[col[e], c0 .. c0+VEC), every slice of the group holding the total
+// sum_{e in [beg, end)} w_e M[col[e], c0 .. c0+VEC), every slice of the group holding the
+// total.  first_j: the group's column indices of the first gw entries (lane lig holds
+// entry beg + lig), already loaded by the caller.
 template <int LANES, int VEC, bool USE_VAL>
 __device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, int64_t beg, int64_t end,
-                                                           const Lanes& L, int slots, bool cok) {
+                                                           const Lanes& L, int slots, bool cok, int first_j) {
   using V = Vec<VEC>;
-  constexpr int UNR = LANES >= 4 ? 8 : 4;
+  constexpr int UNR = LANES == 64 ? GCN_AGG_UNR : (LANES >= 4 ? 8 : 4);
   typename V::T acc = V::zero();
   const float* Mc = p.M + L.c0;
   for (int64_t base = beg; base < end; base += L.gw) {
     const int cnt = (int)((end - base) < L.gw ? (end - base) : L.gw);
-    int my_j = 0;
+    int my_j = first_j;
+    if (base != beg) my_j = L.lig < cnt ? p.col[base + L.lig] : 0;
     float my_w = 0.f;
-    if (L.lig < cnt) {
-      my_j = p.col[base + L.lig];
-      my_w = USE_VAL ? p.val[base + L.lig] : p.dinv[my_j];
-    }
+    if (L.lig < cnt) my_w = USE_VAL ? p.val[base + L.lig] : p.dinv[my_j];
     for (int t = 0; t < cnt; t += slots * UNR) {
       int jj[UNR];
       float ww[UNR];
@@ -126,18 +130,23 @@ __device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, i
       for (int u = 0; u < UNR; ++u) {
         const int e = t + u * slots + L.slot;
         ok[u] = e < cnt;
-        const int src = ok[u] ? e : 0;
-        jj[u] = __shfl(my_j, src, L.gw);
-        ww[u] = __shfl(my_w, src, L.gw);
+        jj[u] = __shfl(my_j, ok[u] ? e : 0, L.gw);
       }
 #pragma unroll
       for (int u = 0; u < UNR; ++u) xs[u] = (ok[u] && cok) ? V::load(Mc + (int64_t)jj[u] * p.ldm) : V::zero();
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) ww[u] = __shfl(my_w, ok[u] ? t + u * slots + L.slot : 0, L.gw);
 #pragma unroll
       for (int u = 0; u < UNR; ++u) V::fma(acc, ok[u] ? ww[u] : 0.f, xs[u]);
     }
   }
   for (int o = LANES; o < L.gw; o <<= 1) V::add_xor(acc, o, L.gw);
   return acc;
+}
+
+template <int LANES>
+__device__ __forceinline__ int load_first_chunk(const AggParams& p, int64_t beg, int64_t end, const Lanes& L) {
+  return (beg + L.lig < end) ? p.col[beg + L.lig] : 0;
 }
 
 // Scale, bias and epilogue of one row; slice 0 writes.
@@ -220,6 +229,8 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
 }
 
 // Every row whose length is at most skip_over (all rows when there is no split plan).
+// One group per row; the hardware overlaps many resident wavefronts, which hides
+// the per-row chain of dependent loads better than prefetching across rows does.
 template <int LANES, int VEC, int EPI, bool USE_VAL>
 __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, int64_t skip_over) {
   const Lanes L = lanes_of<LANES, VEC>(slots);
@@ -228,7 +239,8 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, in
   const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
   if (end - beg > skip_over) return;
   const bool cok = L.c0 < p.w;
-  const auto acc = accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok);
+  const auto acc =
+      accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
   finish_row<LANES, VEC, EPI, USE_VAL>(p, row, acc, L, cok);
 }
 
@@ -245,7 +257,8 @@ __global__ void __launch_bounds__(kBlock) k_chunks(AggParams p, gcn_split sp, in
   const int64_t rend = p.row_ptr[row + 1];
   const int64_t end = beg + GCN_SPLIT_CHUNK < rend ? beg + GCN_SPLIT_CHUNK : rend;
   const bool cok = L.c0 < p.w;
-  const auto acc = accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok);
+  const auto acc =
+      accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
   if (cok && L.slot == 0) Vec<VEC>::store(part + ch * pw + L.c0, acc);
 }
 

@@ -455,8 +455,8 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
     t[2 * l] = gcn_adam_tensor{m->W[l], m->dW[l], m->mW[l], m->vW[l], fi * fo};
     t[2 * l + 1] = gcn_adam_tensor{m->b[l], m->db[l], m->mb[l], m->vb[l], fo};
   }
-  GCN_TRY(launch_adam(t, 2 * L, m->step + 1, m->lr, m->beta1, m->beta2, m->eps, stream));
-  m->step += 1;
+  GCN_TRY(launch_adam(t, 2 * L, m->step + 1, m->d_step, m->lr, m->beta1, m->beta2, m->eps, stream));
+  if (!m->d_step) m->step += 1;
   return GCN_OK;
 }
 
@@ -551,7 +551,17 @@ gcn_status gcn_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, doubl
   for (int i = 0; i < count; ++i)
     if (t[i].count < 0 || (t[i].count > 0 && (!t[i].param || !t[i].grad || !t[i].m || !t[i].v)))
       return fail(GCN_E_INVALID, "gcn_adam: bad tensor");
-  return launch_adam(t, count, step, lr, beta1, beta2, eps, stream);
+  return launch_adam(t, count, step, nullptr, lr, beta1, beta2, eps, stream);
+}
+
+gcn_status gcn_adam_device_step(const gcn_adam_tensor* t, int32_t count, int32_t* d_step, double lr,
+                                double beta1, double beta2, double eps, hipStream_t stream) {
+  g_err.clear();
+  if (count < 0 || (count > 0 && !t) || !d_step) return fail(GCN_E_INVALID, "gcn_adam_device_step: bad arguments");
+  for (int i = 0; i < count; ++i)
+    if (t[i].count < 0 || (t[i].count > 0 && (!t[i].param || !t[i].grad || !t[i].m || !t[i].v)))
+      return fail(GCN_E_INVALID, "gcn_adam_device_step: bad tensor");
+  return launch_adam(t, count, 1, d_step, lr, beta1, beta2, eps, stream);
 }
 
 }  // extern "C"

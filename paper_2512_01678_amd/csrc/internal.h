@@ -141,7 +141,8 @@ gcn_status run_feature_stats(const float* X, int32_t n, int32_t f, int64_t ldx, 
                              int32_t tau_den, int32_t force_mode, int64_t* row_nnz,
                              gcn_feature_info* info, gcn_sparse_x* x, void* ws, hipStream_t s);
 
-gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, double lr, double b1,
-                       double b2, double eps, hipStream_t s);
+// step >= 1 from the host, or (d_step != NULL) read from and incremented on the device
+gcn_status launch_adam(const gcn_adam_tensor* t, int32_t count, int32_t step, int32_t* d_step, double lr,
+                       double b1, double b2, double eps, hipStream_t s);
 
 }  // namespace gcn

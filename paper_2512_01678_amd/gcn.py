@@ -70,7 +70,7 @@ class gcn_model(C.Structure):
     _fields_ = [("n_layers", i32), ("layers", C.POINTER(gcn_layer))] + \
                [(nm, C.POINTER(P)) for nm in ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act",
                                                "saved", "grad")] + \
-               [("lr", f64), ("beta1", f64), ("beta2", f64), ("eps", f64), ("step", i32)]
+               [("lr", f64), ("beta1", f64), ("beta2", f64), ("eps", f64), ("step", i32), ("d_step", P)]
 
 
 class gcn_adam_tensor(C.Structure):
@@ -100,6 +100,7 @@ _SIG = {
     "gcn_spmm": (i32, [i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
     "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
+    "gcn_adam_device_step": (i32, [C.POINTER(gcn_adam_tensor), i32, P, f64, f64, f64, f64, P]),
     "gcn_profile_enable": (i32, [i32]),
     "gcn_profile_count": (i32, []),
     "gcn_profile_read": (i32, [i32, C.POINTER(gcn_profile_record)]),
@@ -348,7 +349,7 @@ class Model:
     """
 
     def __init__(self, n, widths, Ws, bs, device="cuda", x_sparse=False, ld_x=None, lr=0.01,
-                 beta1=0.9, beta2=0.999, eps=1e-8, orders=None):
+                 beta1=0.9, beta2=0.999, eps=1e-8, orders=None, device_step=False):
         self.n = n
         self.widths = tuple(widths)
         L = len(widths) - 1
@@ -400,10 +401,28 @@ class Model:
         for k, v in self._arrays.items():
             setattr(self.c, k, C.cast(v, C.POINTER(P)))
         self.c.lr, self.c.beta1, self.c.beta2, self.c.eps, self.c.step = lr, beta1, beta2, eps, 0
+        self.d_step = torch.zeros(1, dtype=torch.int32, device=dev) if device_step else None
+        self.c.d_step = _ptr(self.d_step)
 
     @property
     def step(self):
-        return self.c.step
+        return int(self.d_step.item()) if self.d_step is not None else self.c.step
+
+    def prepare(self, g: DeviceGraph, X=None, x: SparseFeatures | None = None, labels=None):
+        """Allocate the epoch workspace ahead of time (nothing may allocate during graph capture)."""
+        nbytes = sz(0)
+        _check(_lib.gcn_epoch(C.byref(self.c), C.byref(g.c), _ptr(X), C.byref(x.c) if x is not None else None,
+                              _ptr(labels), _ptr(self.loss), None, C.byref(nbytes), None), "gcn_epoch (size query)")
+        self._ws.get(max(nbytes.value, 256), self.loss.device)
+
+    def epoch_captured(self, g: DeviceGraph, X=None, x: SparseFeatures | None = None, labels=None):
+        """Enqueue one epoch with the prepared workspace and no allocation (for HIP graph capture)."""
+        buf = self._ws.buf
+        nbytes = sz(buf.numel())
+        _check(_lib.gcn_epoch(C.byref(self.c), C.byref(g.c), _ptr(X), C.byref(x.c) if x is not None else None,
+                              _ptr(labels), _ptr(self.loss), buf.data_ptr(), C.byref(nbytes),
+                              P(_stream(None))), "gcn_epoch")
+        return self.loss
 
     def orders(self):
         return [_lib.gcn_layer_order(C.byref(self.layers[l]), int(self.x_sparse and l == 0))

@@ -295,3 +295,86 @@ def test_epoch_rmat_4096_features_sparse(G, orc):
     p.X, p.y = X, gs.labels(n, 32)
     p.Ws, p.bs = gs.make_weights(wl)
     run_epochs(G, orc, p, 1, sparse=True)
+
+
+# ---------------------------------------------------------------------------
+# degenerate cases of the method
+# ---------------------------------------------------------------------------
+
+
+def edge_problem(G, orc, case):
+    rng = np.random.default_rng(17)
+    if case == "no_edges":          # A_hat = I: the GCN is an MLP
+        n, widths = 500, (8, 6, 3)
+        s = d = np.zeros(0, np.int32)
+    elif case == "single_node":
+        n, widths = 1, (4, 3, 2)
+        s = d = np.zeros(0, np.int32)
+    elif case == "width1":          # a one-unit hidden layer
+        n, widths = 300, (5, 1, 4)
+        s, d = gs.chung_lu(n, 900, seed=4)
+    else:                           # all-zero features: s = 1, sparse path with nnz(X) = 0
+        n, widths = 400, (50, 7, 3)
+        s, d = gs.chung_lu(n, 1500, seed=6)
+    p = Problem.__new__(Problem)
+    p.wl = gs.Workload(case, n, "chung_lu", s.size, widths, "normal")
+    p.og, p.dg = orc.build_csr(n, s, d), G.build_csr(n, dev(s), dev(d))
+    X = rng.standard_normal((n, widths[0])).astype(np.float32)
+    if case == "zero_features":
+        X[:] = 0.0
+    p.X = X
+    p.y = rng.integers(0, widths[-1], n).astype(np.int32)
+    p.Ws = [(rng.standard_normal((widths[l], widths[l + 1])) * 0.6).astype(np.float32) for l in range(len(widths) - 1)]
+    p.bs = [(rng.standard_normal(widths[l + 1]) * 0.2).astype(np.float32) for l in range(len(widths) - 1)]
+    return p
+
+
+@pytest.mark.parametrize("case", ["no_edges", "single_node", "width1", "zero_features"])
+def test_epoch_degenerate_cases(G, orc, case):
+    p = edge_problem(G, orc, case)
+    if case == "no_edges":
+        assert p.dg.nnz == p.wl.n
+    run_epochs(G, orc, p, 2, sparse=(case == "zero_features"))
+
+
+# ---------------------------------------------------------------------------
+# one epoch captured in a HIP graph and replayed
+# ---------------------------------------------------------------------------
+
+
+def test_hip_graph_replay_matches_eager(G, small):
+    p = small
+    n = p.wl.n
+    Xd, yd = dev(p.X), dev(p.y)
+    eager = G.Model(n, p.wl.widths, p.Ws, p.bs, device_step=True)
+    graphed = G.Model(n, p.wl.widths, p.Ws, p.bs, device_step=True)
+    graphed.prepare(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    cg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(cg):
+        graphed.epoch_captured(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    for it in range(3):
+        cg.replay()
+        eager.epoch(p.dg, X=Xd, labels=yd)
+        _ = (Xd * 2.0).sum().item()     # unrelated eager work between replays
+        torch.cuda.synchronize()
+        for a, b in zip(graphed.W + graphed.b + graphed.mW + graphed.vW + [graphed.loss],
+                        eager.W + eager.b + eager.mW + eager.vW + [eager.loss]):
+            assert torch.equal(a, b), f"replay {it}"
+    assert graphed.step == eager.step == 3
+
+
+def test_device_step_matches_host_step(G, small):
+    p = small
+    n = p.wl.n
+    Xd, yd = dev(p.X), dev(p.y)
+    a = G.Model(n, p.wl.widths, p.Ws, p.bs, device_step=True)
+    b = G.Model(n, p.wl.widths, p.Ws, p.bs)
+    for _ in range(3):
+        a.epoch(p.dg, X=Xd, labels=yd)
+        b.epoch(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    for x, y in zip(a.W + a.b, b.W + b.b):
+        np.testing.assert_allclose(host(x), host(y), rtol=1e-6, atol=1e-9)
+    assert a.step == b.step == 3
