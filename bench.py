@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--cpu-baseline", default="auto", choices=["auto", "off"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU work budget for the oracle leg")
     ap.add_argument("--no-profile", action="store_true", help="no per-launch events (pure epoch timing)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one epoch in a HIP graph and time K replays (per-launch events off)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead of training, time a plain device copy of this many GiB "
                          "(calibrates HBM counters against a kernel of known traffic)")
@@ -178,15 +180,24 @@ def main():
     if sparse:
         del Xv, Xd  # the sparse path reads only X_csr / X_csc
         torch.cuda.empty_cache()
-    m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x)
+    m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x, device_step=args.graph)
     Xin = None if sparse else Xv
     for _ in range(args.warmup):
         m.epoch(g, X=Xin, x=sx, labels=yd)
     torch.cuda.synchronize()
     print(f"[bench] {args.warmup} warm-up epochs done", file=sys.stderr, flush=True)
 
+    profile = not (args.no_profile or args.graph)
+    cg = None
+    if args.graph:
+        m.prepare(g, X=Xin, x=sx, labels=yd)
+        torch.cuda.synchronize()
+        cg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(cg):
+            m.epoch_captured(g, X=Xin, x=sx, labels=yd)
+        torch.cuda.synchronize()
     launches_per_epoch = 64
-    if not args.no_profile:
+    if profile:
         G.profile_enable(launches_per_epoch * args.steps)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -194,7 +205,10 @@ def main():
     ev0.record(stream)
     t_wall = time.perf_counter()
     for _ in range(args.steps):
-        m.epoch(g, X=Xin, x=sx, labels=yd)
+        if cg is not None:
+            cg.replay()
+        else:
+            m.epoch(g, X=Xin, x=sx, labels=yd)
     ev1.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
@@ -202,11 +216,11 @@ def main():
     ms_per_step = ms_total / args.steps
     loss = float(m.loss.cpu()[0])
     print(f"[bench] {args.steps} epochs: {ms_per_step:.3f} ms/epoch (wall {t_wall * 1e3 / args.steps:.3f}), "
-          f"loss {loss:.5f}", file=sys.stderr, flush=True)
+          f"loss {loss:.5f}, Adam steps {m.step}", file=sys.stderr, flush=True)
 
     # per-launch records -> per-family averages
     fam = {}
-    if not args.no_profile:
+    if profile:
         for r in G.profile_records():
             f = fam.setdefault(r["name"], dict(ms=0.0, count=0, width=r["width"], rows=r["rows"], nnz=r["nnz"]))
             f["ms"] += r["ms"]
@@ -252,7 +266,9 @@ def main():
         "config": {"workload": wl.name, "nodes": wl.n, "nnz_A_plus_I": g.nnz, "widths": list(wl.widths),
                    "feature_path": "sparse" if sparse else "dense", "sparsity": round(info["sparsity"], 6),
                    "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
-                   "per_launch_events": not args.no_profile},
+                   "per_launch_events": profile, "hip_graph": bool(args.graph),
+                   "gemm_mode": "fp32 MFMA" if os.environ.get("GCN_GEMM_MODE") == "fp32"
+                   else "fp32 via exact 3-way bf16 split, 6 bf16 MFMA products"},
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
         "setup_ms": {"csr_build": round(t_csr * 1e3, 2), "density_probe": round(t_probe * 1e3, 2)},
     }

@@ -16,12 +16,40 @@
 // Epilogues: + bias, ReLU, or multiplication by 1[mask > 0]; or, for a
 // split-k launch, a plain store of the partial tile into the workspace, summed
 // afterwards in a fixed order by k_splitk_reduce (deterministic, no atomics).
+//
+// Two arithmetic modes give fp32 results:
+//  * fp32: v_mfma_f32_32x32x2_f32 on the fp32 operands;
+//  * bf16x6 (default): every fp32 operand is split exactly into three bf16 parts
+//    a = a_hi + a_mid + a_lo (24 significant bits, each subtraction exact in
+//    fp32), and the six cross products of order <= 2 (hi.hi, hi.mid, mid.hi,
+//    hi.lo, mid.mid, lo.hi) run on v_mfma_f32_32x32x16_bf16 with fp32
+//    accumulation; bf16 x bf16 products are exact in fp32 and the dropped terms
+//    are below 2^-24 of |a b|, so the result carries fp32 accuracy at 6 bf16
+//    instructions per 32x32x16 step instead of 8 fp32 ones at a quarter of the
+//    rate.
+#include <cstring>
+
 #include "internal.h"
 
 namespace gcn {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// a = hi + mid + lo exactly up to the last part's rounding (round-to-nearest bf16 each)
+__device__ __forceinline__ void split3(const float (&f)[8], bf16x8& hi, bf16x8& mid, bf16x8& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 h = (__bf16)f[e];
+    const float r = f[e] - (float)h;
+    const __bf16 m = (__bf16)r;
+    const float r2 = r - (float)m;
+    hi[e] = h;
+    mid[e] = m;
+    lo[e] = (__bf16)r2;
+  }
+}
 
 constexpr int kPad = 4;
 
@@ -94,7 +122,7 @@ struct Stage {
   }
 };
 
-template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EPI, bool SPLIT>
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EPI, bool SPLIT, bool EMU>
 __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM / 32;
@@ -151,22 +179,52 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
     if (s + 1 < nslab) load_slab(kbeg + (s + 1) * BK);
     const float* la = lds_a(buf);
     const float* lb = lds_b(buf);
-    float af[TM][KH], bf[TN][KH];
+    if constexpr (EMU) {
+      // BK = 16: one 32x32x16 step per slab; lane half h holds k = 8h .. 8h+7
+      bf16x8 ah[TM], am[TM], al[TM], bh[TN], bm[TN], bl[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i) {
+        float f[8];
 #pragma unroll
-      for (int kk = 0; kk < KH; ++kk) af[i][kk] = SA::frag(la, wm * (BM / WM) + i * 32 + l32, h * KH + kk);
+        for (int e = 0; e < 8; ++e) f[e] = SA::frag(la, wm * (BM / WM) + i * 32 + l32, h * 8 + e);
+        split3(f, ah[i], am[i], al[i]);
+      }
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j) {
+        float f[8];
 #pragma unroll
-      for (int kk = 0; kk < KH; ++kk) bf[j][kk] = SB::frag(lb, wn * (BN / WN) + j * 32 + l32, h * KH + kk);
-#pragma unroll
-    for (int kk = 0; kk < KH; ++kk)
+        for (int e = 0; e < 8; ++e) f[e] = SB::frag(lb, wn * (BN / WN) + j * 32 + l32, h * 8 + e);
+        split3(f, bh[j], bm[j], bl[j]);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < TN; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bh[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bm[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bl[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bh[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bm[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bh[j], acc[i][j], 0, 0, 0);
+        }
+    } else {
+      float af[TM][KH], bf[TN][KH];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int kk = 0; kk < KH; ++kk) af[i][kk] = SA::frag(la, wm * (BM / WM) + i * 32 + l32, h * KH + kk);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int kk = 0; kk < KH; ++kk) bf[j][kk] = SB::frag(lb, wn * (BN / WN) + j * 32 + l32, h * KH + kk);
+#pragma unroll
+      for (int kk = 0; kk < KH; ++kk)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
+    }
     if (s + 1 < nslab) {
       sa.store(lds_a(buf ^ 1), tid);
       sb.store(lds_b(buf ^ 1), tid);
@@ -286,33 +344,44 @@ int64_t pick_splits(const GemmParams& p, Shape sh) {
   return s < 1 ? 1 : s;
 }
 
-template <int BM, int BN, int WM, int WN, bool TA, bool TB>
+template <int BM, int BN, int WM, int WN, bool TA, bool TB, bool EMU>
 gcn_status launch_tile(const GemmArgs& g, int64_t splits, hipStream_t s) {
   constexpr int BK = 16;
   dim3 grid((unsigned)ceil_div(g.p.m, BM), (unsigned)ceil_div(g.p.n, BN), (unsigned)splits);
   dim3 block(WM * WN * 64);
   if (splits > 1) {
-    hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, true>), grid, block, 0, s, g);
+    hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, true, EMU>), grid, block, 0, s, g);
   } else {
     switch (g.p.epi) {
       case GEMM_RELU:
-        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_RELU, false>), grid, block, 0, s, g);
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_RELU, false, EMU>), grid, block, 0, s, g);
         break;
       case GEMM_MASK:
-        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_MASK, false>), grid, block, 0, s, g);
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_MASK, false, EMU>), grid, block, 0, s, g);
         break;
       default:
-        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, false>), grid, block, 0, s, g);
+        hipLaunchKernelGGL((k_gemm<BM, BN, BK, WM, WN, TA, TB, GEMM_NONE, false, EMU>), grid, block, 0, s, g);
     }
   }
   return check_launch("gemm");
 }
 
+template <bool TA, bool TB, bool EMU>
+gcn_status launch_shape(const GemmArgs& g, Shape sh, int64_t splits, hipStream_t s) {
+  if (sh.bn == 32) return launch_tile<256, 32, 4, 1, TA, TB, EMU>(g, splits, s);
+  if (sh.bn == 64) return launch_tile<256, 64, 4, 1, TA, TB, EMU>(g, splits, s);
+  return launch_tile<128, 128, 2, 2, TA, TB, EMU>(g, splits, s);
+}
+
 template <bool TA, bool TB>
-gcn_status launch_layout(const GemmArgs& g, Shape sh, int64_t splits, hipStream_t s) {
-  if (sh.bn == 32) return launch_tile<256, 32, 4, 1, TA, TB>(g, splits, s);
-  if (sh.bn == 64) return launch_tile<256, 64, 4, 1, TA, TB>(g, splits, s);
-  return launch_tile<128, 128, 2, 2, TA, TB>(g, splits, s);
+gcn_status launch_layout(const GemmArgs& g, Shape sh, int64_t splits, bool emu, hipStream_t s) {
+  return emu ? launch_shape<TA, TB, true>(g, sh, splits, s) : launch_shape<TA, TB, false>(g, sh, splits, s);
+}
+
+// Arithmetic mode: bf16x6 unless GCN_GEMM_MODE=fp32 (native fp32 MFMA, kept for comparison).
+bool use_emulation() {
+  const char* e = getenv("GCN_GEMM_MODE");
+  return !(e && strcmp(e, "fp32") == 0);
 }
 
 }  // namespace
@@ -340,10 +409,11 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
            (long)p.m, (long)p.n, (long)p.k);
   ProfScope prof(name, (int32_t)p.n, p.m, p.k, s);
   gcn_status st;
-  if (!p.ta && !p.tb) st = launch_layout<false, false>(g, sh, splits, s);
-  else if (!p.ta && p.tb) st = launch_layout<false, true>(g, sh, splits, s);
-  else if (p.ta && !p.tb) st = launch_layout<true, false>(g, sh, splits, s);
-  else st = launch_layout<true, true>(g, sh, splits, s);
+  const bool emu = use_emulation();
+  if (!p.ta && !p.tb) st = launch_layout<false, false>(g, sh, splits, emu, s);
+  else if (!p.ta && p.tb) st = launch_layout<false, true>(g, sh, splits, emu, s);
+  else if (p.ta && !p.tb) st = launch_layout<true, false>(g, sh, splits, emu, s);
+  else st = launch_layout<true, true>(g, sh, splits, emu, s);
   if (st != GCN_OK || splits == 1) return st;
   const int64_t total = p.m * p.n;
   hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, g.part,

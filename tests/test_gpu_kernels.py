@@ -413,3 +413,31 @@ def test_sparse_backward_long_columns(G, orc):
     G.spmm(sx.col_ptr, sx.row[:sx.nnz], sx.cval[:sx.nnz], dev(Q), dW, split=sp)
     ref, mag = orc.spmm(cp, row, cval, Q, want_mag=True)
     assert_mag_close(host(dW), ref, mag, "X_csc Q with long columns")
+
+
+@pytest.mark.parametrize("op", ["NN", "NT", "TN"])
+@pytest.mark.parametrize("shape", [(4000, 256, 256), (3000, 40, 602), (777, 128, 4096), (50000, 64, 100)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_gemm_bf16x6_matches_native_fp32(G, op, shape, monkeypatch):
+    """The bf16x6 split (default) and native fp32 MFMA agree to fp32 accuracy."""
+    m, n, k = shape
+    rng = np.random.default_rng(m + n + k)
+    A = (rng.standard_normal((m, k)) * np.exp(rng.standard_normal((m, 1)))).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    if op == "NN":
+        Ad, Bd, code = dev(A), dev(B), G.OP_NN
+    elif op == "NT":
+        Ad, Bd, code = dev(A), dev(np.ascontiguousarray(B.T)), G.OP_NT
+    else:
+        Ad, Bd, code = dev(np.ascontiguousarray(A.T)), dev(B), G.OP_TN
+    mag = np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64))
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    out = {}
+    for mode in ("bf16x6", "fp32"):
+        monkeypatch.setenv("GCN_GEMM_MODE", mode)
+        C = torch.empty((m, n), dtype=torch.float32, device="cuda")
+        G.gemm(code, Ad, Bd, C)
+        out[mode] = host(C).astype(np.float64)
+        assert_mag_close(out[mode], ref, mag, f"{mode} {op} {shape}")
+    worst = assert_mag_close(out["bf16x6"], out["fp32"], mag, f"bf16x6 vs fp32 {op} {shape}", rtol=2e-6)
+    print(f"bf16x6 vs fp32 {op} {shape}: max |diff| / scale = {worst:.2e}")
