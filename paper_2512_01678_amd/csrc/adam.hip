@@ -27,10 +27,13 @@ struct AdamArgs {
 
 __global__ void __launch_bounds__(256) k_adam(AdamArgs a) {
   const int64_t total = a.off[a.count];
+  // locals, not writes into the argument block: a written argument struct that is also
+  // indexed by tensor would be copied to per-lane scratch memory
+  float bc1 = a.bc1, bc2 = a.bc2;
   if (a.d_step) {
     const double t = (double)(*a.d_step + 1);
-    a.bc1 = (float)(1.0 - pow(a.b1d, t));
-    a.bc2 = (float)(1.0 - pow(a.b2d, t));
+    bc1 = (float)(1.0 - pow(a.b1d, t));
+    bc2 = (float)(1.0 - pow(a.b2d, t));
   }
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * blockDim.x) {
@@ -42,8 +45,8 @@ __global__ void __launch_bounds__(256) k_adam(AdamArgs a) {
     const float v = a.b2 * a.v[t][j] + a.omb2 * (g * g);
     a.m[t][j] = m;
     a.v[t][j] = v;
-    const float mhat = m / a.bc1;
-    const float vhat = v / a.bc2;
+    const float mhat = m / bc1;
+    const float vhat = v / bc2;
     a.p[t][j] -= a.lr * mhat / (sqrtf(vhat) + a.eps);
   }
 }
