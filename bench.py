@@ -52,8 +52,8 @@ def parse():
 
 def alg_bytes_aggregate(nnz: int, rows: int, w: int) -> int:
     """Algorithmic bytes of one normalised aggregation at width w: neighbour-row gathers
-    4 nnz w, column indices 4 nnz, row offsets 8 (rows + 1), dinv 4 rows, output 4 rows w."""
-    return 4 * nnz * w + 4 * nnz + 8 * (rows + 1) + 4 * rows + 4 * rows * w
+    4 nnz w, column indices and entry values 8 nnz, row offsets 8 (rows + 1), output 4 rows w."""
+    return 4 * nnz * w + 8 * nnz + 8 * (rows + 1) + 4 * rows * w
 
 
 def sha_of(path):

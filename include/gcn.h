@@ -92,8 +92,11 @@ typedef struct gcn_split {
 /*
  * Graph operator A_hat in CSR form.  Row i lists the distinct neighbours of
  * node i plus i itself, columns ascending; deg[i] is the row length and
- * dinv[i] = (float)(1 / sqrt((double)deg[i])).  Entry (i, j) of A_hat is
- * dinv[i] * dinv[j]; no value array is stored.
+ * dinv[i] = (float)(1 / sqrt((double)deg[i])).  val holds the entries of
+ * A_hat = D^-1/2 (A + I) D^-1/2 (Section III-A) in CSR order:
+ * val[e] = dinv[i] * dinv[col_idx[e]], one fp32 rounding.  The values are
+ * computed once, when the graph is built, so an aggregation reads each entry's
+ * weight beside its column index instead of gathering dinv of the neighbour.
  */
 typedef struct gcn_graph {
   int32_t n;          /* nodes */
@@ -103,6 +106,7 @@ typedef struct gcn_graph {
   int32_t* col_idx;   /* device, nnz_cap */
   int32_t* deg;       /* device, n */
   float* dinv;        /* device, n */
+  float* val;         /* device, nnz_cap: A_hat entries (set by gcn_build_csr) */
   gcn_split split;    /* hub rows (optional; see gcn_split) */
 } gcn_graph;
 
@@ -146,7 +150,7 @@ typedef struct gcn_layer {
  * d_src, d_dst: n_edges int32 endpoints each (device).  Every pair (u, v) with
  * u != v adds u-v in both directions; pairs with u == v are ignored; repeated
  * pairs count once; each node gets one self-loop.  On entry g->n, g->nnz_cap
- * and the four device pointers must be set; nnz_cap = 2 n_edges + n always
+ * and the five device pointers must be set; nnz_cap = 2 n_edges + n always
  * suffices.  On return g->nnz holds the entry count.  When g->split.rows is
  * non-NULL the hub split plan is built too (g->split.order is left NULL).
  * Errors: GCN_E_RANGE if an endpoint is outside [0, n) (outputs undefined),
@@ -299,13 +303,14 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
  * gcn_spmm -- C[i,:] = sum_e val[e] B[idx[e],:] over compressed rows
  * i < nrows (Section IV-B backend-specialised primitives: X_csr W forward,
  * X^T G from X_csc backward).  Asynchronous.  d_ptr: nrows + 1 int64;
- * d_idx, d_val: d_ptr[nrows] entries with 0 <= idx < b_rows; d_B: b_rows x w
+ * nnz: d_ptr[nrows] as known to the host, used only to shape the launch (-1 if
+ * unknown); d_idx, d_val: d_ptr[nrows] entries with 0 <= idx < b_rows; d_B: b_rows x w
  * (pitch ldb); d_C: nrows x w (pitch ldc).  split: plan of the long rows of this
  * matrix (or NULL); the workspace holds their chunk sums.
  */
-gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, const float* d_val,
-                    int64_t b_rows, int32_t w, const float* d_B, int64_t ldb, float* d_C,
-                    int64_t ldc, const gcn_split* split, void* d_ws, size_t* ws_bytes,
+gcn_status gcn_spmm(int64_t nrows, int64_t nnz, const int64_t* d_ptr, const int32_t* d_idx,
+                    const float* d_val, int64_t b_rows, int32_t w, const float* d_B, int64_t ldb,
+                    float* d_C, int64_t ldc, const gcn_split* split, void* d_ws, size_t* ws_bytes,
                     hipStream_t stream);
 
 /*

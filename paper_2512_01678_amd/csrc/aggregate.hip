@@ -1,10 +1,13 @@
 // aggregate.hip -- row-parallel sparse aggregation on gfx950.
 //
-// Z[u,:] = s_u * sum_{e in row u} w_e * M[col[e], :]  (+ bias, epilogue)
+// Z[u,:] = sum_{e in row u} val[e] * M[col[e], :]  (+ bias, epilogue)
 //
-//  * normalised GCN aggregation (Section III-A): w_e = dinv[col[e]], s_u = dinv[u],
-//    so Z = A_hat M with A_hat = D^-1/2 (A + I) D^-1/2;
-//  * sparse-feature products (Section IV-B): w_e = val[e], s_u = 1 (X_csr W, X_csc G).
+//  * normalised GCN aggregation (Section III-A): val holds the entries of
+//    A_hat = D^-1/2 (A + I) D^-1/2, computed once when the graph is built;
+//  * sparse-feature products (Section IV-B): X_csr W and X_csc G.
+//
+// Each entry's weight is read beside its column index: no per-entry gather of
+// degree data sits between the index load and the neighbour-row gather.
 //
 // Mapping (the paper's row-per-block idea of Algorithm 3, re-cut for 64-wide
 // wavefronts): a slice of LANES lanes covers the row's columns, each lane VEC
@@ -108,7 +111,7 @@ __device__ __forceinline__ Lanes lanes_of(int slots) {
 // sum_{e in [beg, end)} w_e M[col[e], c0 .. c0+VEC), every slice of the group holding the
 // total.  first_j: the group's column indices of the first gw entries (lane lig holds
 // entry beg + lig), already loaded by the caller.
-template <int LANES, int VEC, bool USE_VAL>
+template <int LANES, int VEC>
 __device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, int64_t beg, int64_t end,
                                                            const Lanes& L, int slots, bool cok, int first_j) {
   using V = Vec<VEC>;
@@ -120,7 +123,7 @@ __device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, i
     int my_j = first_j;
     if (base != beg) my_j = L.lig < cnt ? p.col[base + L.lig] : 0;
     float my_w = 0.f;
-    if (L.lig < cnt) my_w = USE_VAL ? p.val[base + L.lig] : p.dinv[my_j];
+    if (L.lig < cnt) my_w = p.val[base + L.lig];
     for (int t = 0; t < cnt; t += slots * UNR) {
       int jj[UNR];
       float ww[UNR];
@@ -149,18 +152,17 @@ __device__ __forceinline__ int load_first_chunk(const AggParams& p, int64_t beg,
   return (beg + L.lig < end) ? p.col[beg + L.lig] : 0;
 }
 
-// Scale, bias and epilogue of one row; slice 0 writes.
-template <int LANES, int VEC, int EPI, bool USE_VAL>
+// Bias and epilogue of one row; slice 0 writes.
+template <int LANES, int VEC, int EPI>
 __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, const typename Vec<VEC>::T& acc,
                                            const Lanes& L, bool cok) {
   using V = Vec<VEC>;
   const int c0 = L.c0;
-  const float s = USE_VAL ? 1.f : p.dinv[row];
   float z[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) {
     const int c = c0 + i;
-    z[i] = s * V::get(acc, i);
+    z[i] = V::get(acc, i);
     if (p.bias && c < p.w) z[i] += p.bias[c];
   }
   if constexpr (EPI == AGG_SOFTMAX) {
@@ -231,7 +233,7 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
 // Every row whose length is at most skip_over (all rows when there is no split plan).
 // One group per row; the hardware overlaps many resident wavefronts, which hides
 // the per-row chain of dependent loads better than prefetching across rows does.
-template <int LANES, int VEC, int EPI, bool USE_VAL>
+template <int LANES, int VEC, int EPI>
 __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, int64_t skip_over) {
   const Lanes L = lanes_of<LANES, VEC>(slots);
   const int64_t row = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
@@ -239,13 +241,12 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, in
   const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
   if (end - beg > skip_over) return;
   const bool cok = L.c0 < p.w;
-  const auto acc =
-      accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
-  finish_row<LANES, VEC, EPI, USE_VAL>(p, row, acc, L, cok);
+  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
+  finish_row<LANES, VEC, EPI>(p, row, acc, L, cok);
 }
 
 // One group per chunk of a long row: partial[ch, :] = sum over the chunk's entries.
-template <int LANES, int VEC, bool USE_VAL>
+template <int LANES, int VEC>
 __global__ void __launch_bounds__(kBlock) k_chunks(AggParams p, gcn_split sp, int slots, float* part, int64_t pw) {
   const Lanes L = lanes_of<LANES, VEC>(slots);
   const int64_t gi = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
@@ -257,13 +258,12 @@ __global__ void __launch_bounds__(kBlock) k_chunks(AggParams p, gcn_split sp, in
   const int64_t rend = p.row_ptr[row + 1];
   const int64_t end = beg + GCN_SPLIT_CHUNK < rend ? beg + GCN_SPLIT_CHUNK : rend;
   const bool cok = L.c0 < p.w;
-  const auto acc =
-      accumulate<LANES, VEC, USE_VAL>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
+  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
   if (cok && L.slot == 0) Vec<VEC>::store(part + ch * pw + L.c0, acc);
 }
 
 // One group per long row: add its chunk sums in chunk order, then the row epilogue.
-template <int LANES, int VEC, int EPI, bool USE_VAL>
+template <int LANES, int VEC, int EPI>
 __global__ void __launch_bounds__(kBlock) k_combine(AggParams p, gcn_split sp, int slots, const float* part,
                                                     int64_t pw) {
   using V = Vec<VEC>;
@@ -274,7 +274,7 @@ __global__ void __launch_bounds__(kBlock) k_combine(AggParams p, gcn_split sp, i
   typename V::T acc = V::zero();
   if (cok)
     for (int64_t ch = sp.first[h]; ch < sp.first[h + 1]; ++ch) V::add(acc, V::load(part + ch * pw + L.c0));
-  finish_row<LANES, VEC, EPI, USE_VAL>(p, sp.rows[h], acc, L, cok);
+  finish_row<LANES, VEC, EPI>(p, sp.rows[h], acc, L, cok);
 }
 
 struct Launch {
@@ -286,8 +286,8 @@ struct Launch {
   hipStream_t s;
 };
 
-template <int LANES, int VEC, int EPI, bool USE_VAL>
-gcn_status launch4(const Launch& a) {
+template <int LANES, int VEC, int EPI>
+gcn_status launch3(const Launch& a) {
   const AggParams& p = *a.p;
   const bool split = has_split(a.sp);
   const int64_t skip = split ? (int64_t)GCN_SPLIT_MIN : INT64_MAX;
@@ -295,31 +295,23 @@ gcn_status launch4(const Launch& a) {
   {
     const int gw = LANES * a.slots;
     dim3 grid((unsigned)ceil_div(p.n, kBlock / gw), gy);
-    hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, a.slots, skip);
+    hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI>), grid, dim3(kBlock), 0, a.s, p, a.slots, skip);
     GCN_TRY(check_launch("aggregate"));
   }
   if (!split) return GCN_OK;
   {
     const int gw = LANES * a.chunk_slots;
     dim3 grid((unsigned)ceil_div(a.sp->n_chunk, kBlock / gw), gy);
-    hipLaunchKernelGGL((k_chunks<LANES, VEC, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, *a.sp, a.chunk_slots,
+    hipLaunchKernelGGL((k_chunks<LANES, VEC>), grid, dim3(kBlock), 0, a.s, p, *a.sp, a.chunk_slots,
                        a.part, a.pw);
     GCN_TRY(check_launch("aggregate chunks"));
   }
   {
     dim3 grid((unsigned)ceil_div(a.sp->n_long, kBlock / LANES), gy);
-    hipLaunchKernelGGL((k_combine<LANES, VEC, EPI, USE_VAL>), grid, dim3(kBlock), 0, a.s, p, *a.sp, 1, a.part,
+    hipLaunchKernelGGL((k_combine<LANES, VEC, EPI>), grid, dim3(kBlock), 0, a.s, p, *a.sp, 1, a.part,
                        a.pw);
     return check_launch("aggregate combine");
   }
-}
-
-template <int LANES, int VEC, int EPI>
-gcn_status launch3(const Launch& a) {
-  if constexpr (EPI == AGG_NONE) {
-    if (a.p->val) return launch4<LANES, VEC, EPI, true>(a);
-  }
-  return launch4<LANES, VEC, EPI, false>(a);
 }
 
 template <int LANES, int VEC>
@@ -345,7 +337,7 @@ gcn_status launch1(const Launch& a, int lanes) {
   }
 }
 
-// Neighbour slices per row: as many as keep at least 2 neighbours per slice on an
+// Neighbour slices per row: as many as keep at least one neighbour per slice on an
 // average row (slices beyond that would mostly idle), within one wavefront.
 int pick_slots(int lanes, int64_t nnz, int64_t rows) {
   const int max_slots = std::min(64 / lanes, 16);
@@ -357,7 +349,7 @@ int pick_slots(int lanes, int64_t nnz, int64_t rows) {
   if (nnz < 0 || rows <= 0) return 1;
   const double avg = (double)nnz / (double)rows;
   int s = 1;
-  while (s * 2 <= max_slots && 2.0 * (s * 2) <= avg) s *= 2;
+  while (s * 2 <= max_slots && s * 2 <= avg) s *= 2;
   return s;
 }
 
@@ -393,7 +385,7 @@ gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* sp
   a.chunk_slots = std::min(64 / lanes, 16);
   a.s = s;
   char name[64];
-  snprintf(name, sizeof name, "%s_w%d", p.tag ? p.tag : (p.val ? "spmm" : "aggregate"), p.w);
+  snprintf(name, sizeof name, "%s_w%d", p.tag ? p.tag : "aggregate", p.w);
   ProfScope prof(name, p.w, p.n, nnz, s);
   return vec4 ? launch1<4>(a, lanes) : launch1<1>(a, lanes);
 }

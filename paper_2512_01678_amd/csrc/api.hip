@@ -44,7 +44,7 @@ gcn_status ws_protocol(void* d_ws, size_t* ws_bytes, size_t need, const char* wh
 gcn_status check_graph(const gcn_graph* g, const char* who) {
   if (!g) return fail(GCN_E_INVALID, std::string(who) + ": graph is NULL");
   if (g->n < 0) return fail(GCN_E_INVALID, std::string(who) + ": negative node count");
-  if (g->n > 0 && (!g->row_ptr || !g->col_idx || !g->dinv))
+  if (g->n > 0 && (!g->row_ptr || !g->col_idx || !g->val))
     return fail(GCN_E_INVALID, std::string(who) + ": graph arrays missing");
   if (g->split.rows && g->split.n_long > 0 && (!g->split.first || !g->split.owner))
     return fail(GCN_E_INVALID, std::string(who) + ": split plan arrays missing");
@@ -91,7 +91,7 @@ AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, 
   p.n = g->n;
   p.row_ptr = g->row_ptr;
   p.col = g->col_idx;
-  p.dinv = g->dinv;
+  p.val = g->val;
   p.M = M;
   p.ldm = ldm;
   p.w = w;
@@ -313,7 +313,7 @@ const char* gcn_status_string(gcn_status s) {
 
 const char* gcn_last_error(void) { return g_err.c_str(); }
 
-int32_t gcn_version(void) { return 1; }
+int32_t gcn_version(void) { return 2; }
 
 int32_t gcn_layer_order(const gcn_layer* L, int32_t x_sparse) {
   return L ? resolve_order(L, x_sparse != 0) : GCN_TRANSFORM_FIRST;
@@ -330,7 +330,7 @@ gcn_status gcn_build_csr(int32_t n, int64_t n_edges, const int32_t* d_src, const
   if (query) return GCN_OK;
   if (!g) return fail(GCN_E_INVALID, "gcn_build_csr: graph is NULL");
   if (n_edges > 0 && (!d_src || !d_dst)) return fail(GCN_E_INVALID, "gcn_build_csr: edge arrays missing");
-  if (!g->row_ptr || (n > 0 && (!g->deg || !g->dinv || !g->col_idx)))
+  if (!g->row_ptr || (n > 0 && (!g->deg || !g->dinv || !g->col_idx || !g->val)))
     return fail(GCN_E_INVALID, "gcn_build_csr: output arrays missing");
   if (g->split.rows && (!g->split.first || !g->split.owner || g->split.cap < 0))
     return fail(GCN_E_INVALID, "gcn_build_csr: split plan arrays missing");
@@ -504,9 +504,10 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
   return launch_gemm(p, d_ws, stream);
 }
 
-gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, const float* d_val,
-                    int64_t b_rows, int32_t w, const float* d_B, int64_t ldb, float* d_C, int64_t ldc,
-                    const gcn_split* split, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+gcn_status gcn_spmm(int64_t nrows, int64_t nnz, const int64_t* d_ptr, const int32_t* d_idx,
+                    const float* d_val, int64_t b_rows, int32_t w, const float* d_B, int64_t ldb,
+                    float* d_C, int64_t ldc, const gcn_split* split, void* d_ws, size_t* ws_bytes,
+                    hipStream_t stream) {
   g_err.clear();
   if (nrows < 0 || nrows > INT32_MAX || w < 0 || b_rows < 0 || ldb < w || ldc < w)
     return fail(GCN_E_INVALID, "gcn_spmm: bad size or pitch");
@@ -528,7 +529,8 @@ gcn_status gcn_spmm(int64_t nrows, const int64_t* d_ptr, const int32_t* d_idx, c
   p.Z = d_C;
   p.ldz = ldc;
   p.epi = AGG_NONE;
-  return launch_aggregate(p, -1, split, d_ws, stream);
+  p.tag = "spmm";
+  return launch_aggregate(p, nnz, split, d_ws, stream);
 }
 
 gcn_status gcn_column_sums(int64_t rows, int32_t w, const float* d_G, int64_t ldg, float* d_out,

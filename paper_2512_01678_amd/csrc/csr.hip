@@ -16,6 +16,7 @@
 //                        workspace, read back in column order.
 //  5. scan the unique counts (the degrees) into row_ptr; compact into col_idx
 //     and write dinv = (float)(1 / sqrt((double)deg)).
+//  6. write the entries of A_hat, val[e] = dinv[row] * dinv[col[e]] (fp32).
 #include "internal.h"
 
 namespace gcn {
@@ -265,6 +266,15 @@ __global__ void __launch_bounds__(256) k_compact(int32_t n, const int64_t* raw_o
   if (lane == 0) dinv[row] = (float)(1.0 / sqrt((double)d));
 }
 
+__global__ void __launch_bounds__(256) k_values(int32_t n, const int64_t* row_ptr, const int32_t* col_idx,
+                                                const float* dinv, float* val) {
+  const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / 64;
+  const int lane = threadIdx.x % 64;
+  if (row >= n) return;
+  const float di = dinv[row];
+  for (int64_t e = row_ptr[row] + lane; e < row_ptr[row + 1]; e += 64) val[e] = di * dinv[col_idx[e]];
+}
+
 }  // namespace
 
 size_t build_csr_workspace(int32_t n, int64_t n_edges) {
@@ -329,6 +339,9 @@ gcn_status run_build_csr(int32_t n, int64_t n_edges, const int32_t* src, const i
     hipLaunchKernelGGL(k_compact, dim3((unsigned)ceil_div(n, 4)), dim3(256), 0, s, n, w.raw_off, w.raw,
                        g->row_ptr, g->deg, g->col_idx, g->dinv);
     GCN_TRY(check_launch("csr compact"));
+    hipLaunchKernelGGL(k_values, dim3((unsigned)ceil_div(n, 4)), dim3(256), 0, s, n, g->row_ptr, g->col_idx,
+                       g->dinv, g->val);
+    GCN_TRY(check_launch("csr values"));
   }
   g->split.order = nullptr;
   if (g->split.rows) GCN_TRY(build_split(g->row_ptr, n, &g->split, false, w.split, s));

@@ -72,8 +72,7 @@ struct AggParams {
   int32_t n;               // output rows
   const int64_t* row_ptr;  // n + 1
   const int32_t* col;      // neighbours / column indices
-  const float* dinv;       // normalised aggregation: dinv weights (else NULL)
-  const float* val;        // stored values (sparse products), else NULL
+  const float* val;        // entry values (A_hat, or X in CSR / CSC form)
   const float* M;          // gathered rows
   int64_t ldm;
   int32_t w;

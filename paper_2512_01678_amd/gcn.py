@@ -49,7 +49,7 @@ class gcn_split(C.Structure):
 
 class gcn_graph(C.Structure):
     _fields_ = [("n", i32), ("nnz", i64), ("nnz_cap", i64), ("row_ptr", P), ("col_idx", P),
-                ("deg", P), ("dinv", P), ("split", gcn_split)]
+                ("deg", P), ("dinv", P), ("val", P), ("split", gcn_split)]
 
 
 class gcn_sparse_x(C.Structure):
@@ -97,7 +97,7 @@ _SIG = {
                         P, C.POINTER(sz), P]),
     "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i32, P, i64, P, i64, P, C.POINTER(sz), P]),
     "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
-    "gcn_spmm": (i32, [i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
+    "gcn_spmm": (i32, [i64, i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
     "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
     "gcn_adam_device_step": (i32, [C.POINTER(gcn_adam_tensor), i32, P, f64, f64, f64, f64, P]),
@@ -184,13 +184,13 @@ class SplitPlan:
 class DeviceGraph:
     """A + I in CSR on the device (owning torch tensors), with its hub split plan."""
 
-    def __init__(self, n, row_ptr, col_idx, deg, dinv, nnz, plan: SplitPlan | None, split_c):
+    def __init__(self, n, row_ptr, col_idx, deg, dinv, val, nnz, plan: SplitPlan | None, split_c):
         self.n = n
-        self.row_ptr, self.col_idx, self.deg, self.dinv = row_ptr, col_idx, deg, dinv
+        self.row_ptr, self.col_idx, self.deg, self.dinv, self.val = row_ptr, col_idx, deg, dinv, val
         self.nnz = nnz
         self.plan = plan
         self.c = gcn_graph(n, nnz, col_idx.numel(), _ptr(row_ptr), _ptr(col_idx), _ptr(deg), _ptr(dinv),
-                           split_c)
+                           _ptr(val), split_c)
 
     @property
     def n_long(self):
@@ -205,12 +205,13 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None, split: 
     col = torch.empty(max(2 * ne + n, 1), dtype=torch.int32, device=dev)
     deg = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
     dinv = torch.empty(max(n, 1), dtype=torch.float32, device=dev)
+    val = torch.empty(col.numel(), dtype=torch.float32, device=dev)
     plan = SplitPlan(2 * ne + n, dev, order=False) if split else None
-    g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv),
+    g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv), _ptr(val),
                   plan.c if plan else gcn_split())
     _run_ws(_lib.gcn_build_csr, (n, ne, _ptr(src), _ptr(dst), C.byref(g)), (P(_stream(stream)),),
             "gcn_build_csr", None, dev)
-    return DeviceGraph(n, row_ptr, col, deg, dinv, g.nnz, plan, g.split)
+    return DeviceGraph(n, row_ptr, col, deg, dinv, val, g.nnz, plan, g.split)
 
 
 class SparseFeatures:
@@ -289,8 +290,8 @@ def gemm(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, ws: _Workspace | Non
 
 def spmm(ptr, idx, val, B, out, split: gcn_split | None = None, stream=None):
     nrows = ptr.numel() - 1
-    _run_ws(_lib.gcn_spmm, (nrows, _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B), _ld(B),
-                            _ptr(out), _ld(out), C.byref(split) if split is not None else None),
+    _run_ws(_lib.gcn_spmm, (nrows, idx.numel(), _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B),
+                            _ld(B), _ptr(out), _ld(out), C.byref(split) if split is not None else None),
             (P(_stream(stream)),), "gcn_spmm", None, out.device)
     return out
 

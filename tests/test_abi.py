@@ -70,7 +70,7 @@ def test_status_strings(G):
     assert L.gcn_status_string(0) == b"GCN_OK"
     assert L.gcn_status_string(-4) == b"GCN_E_CAPACITY"
     assert L.gcn_status_string(-99) == b"GCN_E_UNKNOWN"
-    assert L.gcn_version() >= 1
+    assert L.gcn_version() >= 2
 
 
 def test_host_validation_rejects_bad_calls(G):
@@ -86,7 +86,7 @@ def test_host_validation_rejects_bad_calls(G):
     assert L.gcn_build_csr(10, 5, None, None, None, None, None, None) == G.E_INVALID
     # a workspace that is too small is a capacity error, before any launch
     small = G.sz(8)
-    g = G.gcn_graph(10, 0, 100, 1, 1, 1, 1)
+    g = G.gcn_graph(10, 0, 100, 1, 1, 1, 1, 1)
     assert L.gcn_build_csr(10, 5, 1, 1, C.byref(g), 1, C.byref(small), None) == G.E_CAPACITY
     assert "needed" in L.gcn_last_error().decode()
     # feature stats: bad tau, pitch < width, bad force mode
@@ -101,19 +101,23 @@ def test_host_validation_rejects_bad_calls(G):
     assert L.gcn_gemm(G.OP_NN, 4, 4, 4, None, 4, 1, 4, 1, 4, None, 0, None, 0, 1, C.byref(nb2), None) == G.E_INVALID
     # aggregate: NULL graph, mask epilogue without mask
     assert L.gcn_aggregate(None, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
-    g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1)
+    g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1)
     assert L.gcn_aggregate(C.byref(g2), 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None, C.byref(nb),
                            None) == G.E_INVALID
     assert L.gcn_aggregate(C.byref(g2), 4, 1, 3, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    # the entries of A_hat are required
+    noval = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, None)
+    assert L.gcn_aggregate(C.byref(noval), 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_build_csr(10, 5, 1, 1, C.byref(noval), 1, C.byref(G.sz(1 << 20)), None) == G.E_INVALID
     # a split plan with long rows needs its chunk sums in the workspace
     sp = G.gcn_split(3, 50, 64, 1, 1, 1, None)
-    g3 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, sp)
+    g3 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1, sp)
     assert L.gcn_aggregate(C.byref(g3), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.OK
     assert nb.value == 50 * 40 * 4
-    bad = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, G.gcn_split(3, 50, 64, 1, None, 1, None))
+    bad = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1, G.gcn_split(3, 50, 64, 1, None, 1, None))
     assert L.gcn_aggregate(C.byref(bad), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.E_INVALID
     # spmm: bad pitch
-    assert L.gcn_spmm(10, 1, 1, 1, 5, 8, 1, 7, 1, 8, None, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_spmm(10, 20, 1, 1, 1, 5, 8, 1, 7, 1, 8, None, None, C.byref(nb), None) == G.E_INVALID
     # adam: step 0, too many tensors
     assert L.gcn_adam(None, 0, 0, 0.01, 0.9, 0.999, 1e-8, None) == G.E_INVALID
     arr = (G.gcn_adam_tensor * 17)()
@@ -126,7 +130,7 @@ def test_host_validation_rejects_bad_calls(G):
 def test_layer_validation(G):
     L = G.raw_lib()
     nb = G.sz(0)
-    g = G.gcn_graph(10, 20, 20, 1, 1, 1, 1)
+    g = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1)
     lay = G.gcn_layer(8, 4, 8, 4, G.ACT_RELU, G.ORDER_AUTO, 1)
     # neither / both inputs
     assert L.gcn_layer_fwd(C.byref(g), C.byref(lay), None, None, 1, 1, 1, None, None, None, None, None,

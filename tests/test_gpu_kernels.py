@@ -49,6 +49,11 @@ def check_graph_equal(dg, og, n):
     np.testing.assert_array_equal(host(dg.col_idx)[:og.nnz], og.col_idx)
     np.testing.assert_array_equal(host(dg.deg)[:n], og.deg)
     np.testing.assert_array_equal(host(dg.dinv)[:n].view(np.int32), og.dinv.view(np.int32))
+    # stored entries of A_hat: fl32(dinv[i] * dinv[j]), one IEEE rounding
+    rows = np.repeat(np.arange(n), np.diff(og.row_ptr))
+    want = og.dinv[rows] * og.dinv[og.col_idx]
+    assert want.dtype == np.float32
+    np.testing.assert_array_equal(host(dg.val)[:og.nnz].view(np.int32), want.view(np.int32))
 
 
 @pytest.mark.parametrize("case", adversarial_graphs(), ids=lambda c: c[0])
