@@ -26,7 +26,10 @@
 //    accumulation; bf16 x bf16 products are exact in fp32 and the dropped terms
 //    are below 2^-24 of |a b|, so the result carries fp32 accuracy at 6 bf16
 //    instructions per 32x32x16 step instead of 8 fp32 ones at a quarter of the
-//    rate.
+//    rate.  The split happens once per element, when a slab is staged: LDS holds
+//    three k-contiguous bf16 planes, so the wavefronts that share an operand row
+//    do not each redo it (vector ALU time, not the matrix cores, bounds this
+//    product on gfx950), and every fragment is one 16-byte LDS read.
 #include <cstring>
 
 #include "internal.h"
@@ -37,21 +40,8 @@ namespace {
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-// a = hi + mid + lo exactly up to the last part's rounding (round-to-nearest bf16 each)
-__device__ __forceinline__ void split3(const float (&f)[8], bf16x8& hi, bf16x8& mid, bf16x8& lo) {
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const __bf16 h = (__bf16)f[e];
-    const float r = f[e] - (float)h;
-    const __bf16 m = (__bf16)r;
-    const float r2 = r - (float)m;
-    hi[e] = h;
-    mid[e] = m;
-    lo[e] = (__bf16)r2;
-  }
-}
-
 constexpr int kPad = 4;
+
 
 struct GemmArgs {
   GemmParams p;
@@ -83,7 +73,20 @@ struct Stage {
   static constexpr int kPer = (kChunks + NT - 1) / NT;
   static constexpr int kLdsFloats = KCONT ? R * (BK + kPad) : BK * (R + kPad);
   float4 reg[kPer];
+  const float* src_;
+  int64_t ld_, r0_, rlim_, kend_;
+  bool vec_;
 
+  __device__ __forceinline__ void prepare(const float* src, int64_t ld, int64_t r0, int64_t rlim,
+                                          int64_t kend, bool vec, int) {
+    src_ = src;
+    ld_ = ld;
+    r0_ = r0;
+    rlim_ = rlim;
+    kend_ = kend;
+    vec_ = vec;
+  }
+  __device__ __forceinline__ void load(int64_t k0, int tid) { load(src_, ld_, r0_, rlim_, k0, kend_, vec_, tid); }
   __device__ __forceinline__ void load(const float* src, int64_t ld, int64_t r0, int64_t rlim,
                                        int64_t k0, int64_t klim, bool vec, int tid) {
 #pragma unroll
@@ -122,21 +125,158 @@ struct Stage {
   }
 };
 
+// Two round-to-nearest bf16 values packed in one dword (a in the low half).
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  const f2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
+}
+
+// Exact three-way split of a pair: a = hi + mid + lo (each part a bf16), packed per part.
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+  hi = pk_bf16(a, b);
+  const float ra = a - __uint_as_float(hi << 16), rb = b - __uint_as_float(hi & 0xffff0000u);
+  mid = pk_bf16(ra, rb);
+  lo = pk_bf16(ra - __uint_as_float(mid << 16), rb - __uint_as_float(mid & 0xffff0000u));
+}
+
+// Staging of one operand slab for the bf16x6 mode: every element is split once, when
+// the slab goes into LDS, into three bf16 planes laid out k-contiguous,
+// [plane][R][BK + 8], so that a fragment (8 consecutive k of one row) is one 16-byte
+// read.  Each thread loads 4 consecutive k of one row: a 16-byte vector when k is
+// contiguous in memory, else 4 dwords that are coalesced across the lanes (consecutive
+// lanes take consecutive rows).  A thread's byte offsets inside the tile are fixed for
+// the whole k walk, so a slab load is a wave-uniform base plus those 32-bit offsets
+// (no per-slab address arithmetic); rows past the edge of the matrix re-read its last
+// row (their outputs are never stored); only a partial last slab checks k.
+template <int R, int BK, int NT, bool KCONT>
+struct StageX {
+  static constexpr int kChunks = R * BK / 4;
+  static constexpr int kPer = (kChunks + NT - 1) / NT;
+  static constexpr int kPitch = BK + 8;  // bf16 per plane row (16-byte multiple)
+  static constexpr int kPlane = R * kPitch;
+  static constexpr int kLdsFloats = 3 * kPlane / 2;
+  float4 reg[kPer];
+  uint32_t off[kPer];  // byte offset of the chunk's first element from the slab base
+  const char* src;
+  int64_t ld, r0, kend;
+  bool vec;
+
+  static __device__ __forceinline__ void coords(int c, int& r, int& kq) {
+    if (KCONT) {
+      r = c / (BK / 4);
+      kq = (c % (BK / 4)) * 4;
+    } else {
+      r = c % R;
+      kq = (c / R) * 4;
+    }
+  }
+  __device__ __forceinline__ void prepare(const float* src_, int64_t ld_, int64_t r0_, int64_t rlim,
+                                          int64_t kend_, bool vec_, int tid) {
+    src = reinterpret_cast<const char*>(src_);
+    ld = ld_;
+    r0 = r0_;
+    kend = kend_;
+    vec = vec_;
+    const int64_t last = rlim - 1 - r0_;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      int r, kq;
+      coords(tid + i * NT, r, kq);
+      const int64_t rr = r < last ? r : last;
+      off[i] = (uint32_t)(4 * (KCONT ? rr * ld + kq : kq * ld + rr));
+    }
+  }
+  __device__ __forceinline__ void load(int64_t k0, int tid) {
+    const char* base = src + 4 * (KCONT ? r0 * ld + k0 : k0 * ld + r0);
+    const int64_t kleft = kend - k0;  // >= 1
+    if (kleft >= BK && (vec || !KCONT)) {
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        if (kChunks % NT == 0 || tid + i * NT < kChunks) {
+          if (KCONT) {
+            reg[i] = *reinterpret_cast<const float4*>(base + off[i]);
+          } else {
+            const char* q = base + off[i];
+            reg[i].x = *reinterpret_cast<const float*>(q);
+            reg[i].y = *reinterpret_cast<const float*>(q + 4 * ld);
+            reg[i].z = *reinterpret_cast<const float*>(q + 8 * ld);
+            reg[i].w = *reinterpret_cast<const float*>(q + 12 * ld);
+          }
+        }
+      }
+    } else {
+      // partial last slab, or unaligned k-contiguous rows: element by element
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        reg[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        int r, kq;
+        coords(tid + i * NT, r, kq);
+        if (kChunks % NT == 0 || tid + i * NT < kChunks) {
+          const char* q = base + off[i];
+          const int64_t step = KCONT ? 4 : 4 * ld;
+          if (kq + 0 < kleft) reg[i].x = *reinterpret_cast<const float*>(q);
+          if (kq + 1 < kleft) reg[i].y = *reinterpret_cast<const float*>(q + step);
+          if (kq + 2 < kleft) reg[i].z = *reinterpret_cast<const float*>(q + 2 * step);
+          if (kq + 3 < kleft) reg[i].w = *reinterpret_cast<const float*>(q + 3 * step);
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void store(float* lds_f, int tid) const {
+    __bf16* lds = reinterpret_cast<__bf16*>(lds_f);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = tid + i * NT;
+      if (kChunks % NT == 0 || c < kChunks) {
+        int r, kq;
+        coords(c, r, kq);
+        uint2 hi, mid, lo;
+        split_pair(reg[i].x, reg[i].y, hi.x, mid.x, lo.x);
+        split_pair(reg[i].z, reg[i].w, hi.y, mid.y, lo.y);
+        __bf16* d = lds + r * kPitch + kq;
+        *reinterpret_cast<uint2*>(d) = hi;
+        *reinterpret_cast<uint2*>(d + kPlane) = mid;
+        *reinterpret_cast<uint2*>(d + 2 * kPlane) = lo;
+      }
+    }
+  }
+  // 8 consecutive k (from kofs) of sub-tile row rr in plane pl
+  static __device__ __forceinline__ bf16x8 frag(const float* lds_f, int pl, int rr, int kofs) {
+    const __bf16* lds = reinterpret_cast<const __bf16*>(lds_f);
+    return *reinterpret_cast<const bf16x8*>(lds + pl * kPlane + rr * kPitch + kofs);
+  }
+};
+
+template <bool EMU, int R, int BK, int NT, bool KCONT>
+struct StageFor {
+  using T = Stage<R, BK, NT, KCONT>;
+};
+template <int R, int BK, int NT, bool KCONT>
+struct StageFor<true, R, BK, NT, KCONT> {
+  using T = StageX<R, BK, NT, KCONT>;
+};
+
 template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, int EPI, bool SPLIT, bool EMU>
 __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   constexpr int NT = WM * WN * 64;
   constexpr int TM = BM / WM / 32;
   constexpr int TN = BN / WN / 32;
   constexpr int KH = BK / 2;
-  using SA = Stage<BM, BK, NT, !TA>;  // A(m,k): k-contiguous unless transposed
-  using SB = Stage<BN, BK, NT, TB>;   // B(k,n): n-contiguous unless transposed
+  using SA = typename StageFor<EMU, BM, BK, NT, !TA>::T;  // A(m,k): k-contiguous unless transposed
+  using SB = typename StageFor<EMU, BN, BK, NT, TB>::T;   // B(k,n): n-contiguous unless transposed
+  // LDS buffers per operand: two for fp32 slabs (the next slab is stored while the
+  // current one is read); one for the larger bf16 planes (the next slab waits in
+  // registers behind an extra barrier), which leaves room for more workgroups per CU
+  constexpr int NBUF = EMU ? 1 : 2;
   constexpr int kA = SA::kLdsFloats, kB = SB::kLdsFloats;
   constexpr int RB = BM / WM;               // rows of one epilogue round
   constexpr int kEpi = RB * (BN + kPad);
-  constexpr int kTot = 2 * (kA + kB) > kEpi ? 2 * (kA + kB) : kEpi;
+  constexpr int kTot = NBUF * (kA + kB) > kEpi ? NBUF * (kA + kB) : kEpi;
   __shared__ __attribute__((aligned(16))) float smem[kTot];
-  auto lds_a = [&](int b) { return smem + b * kA; };
-  auto lds_b = [&](int b) { return smem + 2 * kA + b * kB; };
+  auto lds_a = [&](int b) { return smem + (b % NBUF) * kA; };
+  auto lds_b = [&](int b) { return smem + NBUF * kA + (b % NBUF) * kB; };
 
   const GemmParams& p = g.p;
   const int tid = threadIdx.x;
@@ -162,9 +302,11 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   SA sa;
   SB sb;
   // A operand: rows m, cols k.  TA: stored k x m.
+  sa.prepare(p.A, p.lda, m0, p.m, kend, g.a_vec, tid);
+  sb.prepare(p.B, p.ldb, n0, p.n, kend, g.b_vec, tid);
   auto load_slab = [&](int64_t k0) {
-    sa.load(p.A, p.lda, m0, p.m, k0, kend, g.a_vec, tid);
-    sb.load(p.B, p.ldb, n0, p.n, k0, kend, g.b_vec, tid);
+    sa.load(k0, tid);
+    sb.load(k0, tid);
   };
 
   const int64_t nslab = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
@@ -180,33 +322,38 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
     const float* la = lds_a(buf);
     const float* lb = lds_b(buf);
     if constexpr (EMU) {
-      // BK = 16: one 32x32x16 step per slab; lane half h holds k = 8h .. 8h+7
-      bf16x8 ah[TM], am[TM], al[TM], bh[TN], bm[TN], bl[TN];
+      // BK / 16 steps of 32x32x16 per slab; in step t lane half h holds
+      // k = h * BK / 2 + 8 t .. + 7 of both operands
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        float f[8];
+      for (int t = 0; t < BK / 16; ++t) {
+        bf16x8 ah[TM], am[TM], al[TM], bh[TN], bm[TN], bl[TN];
+        const int kofs = h * KH + 8 * t;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = SA::frag(la, wm * (BM / WM) + i * 32 + l32, h * 8 + e);
-        split3(f, ah[i], am[i], al[i]);
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = SB::frag(lb, wn * (BN / WN) + j * 32 + l32, h * 8 + e);
-        split3(f, bh[j], bm[j], bl[j]);
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
+        for (int i = 0; i < TM; ++i) {
+          const int rr = wm * (BM / WM) + i * 32 + l32;
+          ah[i] = SA::frag(la, 0, rr, kofs);
+          am[i] = SA::frag(la, 1, rr, kofs);
+          al[i] = SA::frag(la, 2, rr, kofs);
+        }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bh[j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bm[j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bl[j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bh[j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bm[j], acc[i][j], 0, 0, 0);
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bh[j], acc[i][j], 0, 0, 0);
+          const int rr = wn * (BN / WN) + j * 32 + l32;
+          bh[j] = SB::frag(lb, 0, rr, kofs);
+          bm[j] = SB::frag(lb, 1, rr, kofs);
+          bl[j] = SB::frag(lb, 2, rr, kofs);
         }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bh[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bm[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bl[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bh[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bm[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bh[j], acc[i][j], 0, 0, 0);
+          }
+      }
     } else {
       float af[TM][KH], bf[TN][KH];
 #pragma unroll
@@ -225,6 +372,7 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
           for (int j = 0; j < TN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[i][kk], bf[j][kk], acc[i][j], 0, 0, 0);
     }
+    if (NBUF == 1) __syncthreads();  // every wave is done with the only buffer
     if (s + 1 < nslab) {
       sa.store(lds_a(buf ^ 1), tid);
       sb.store(lds_b(buf ^ 1), tid);
@@ -328,9 +476,13 @@ struct Shape {
   int bm, bn;
 };
 
-Shape pick_shape(const GemmParams& p) {
-  if (p.n <= 32) return {256, 32};
-  if (p.n <= 64) return {256, 64};
+// 128 x 128 tiles (2 x 2 wavefronts) for wide outputs; for narrow ones BM x 32 or BM x 64
+// tiles of BM / 64 wavefronts stacked along m: 256 rows in fp32 mode, 128 in bf16x6 mode
+// (whose larger LDS slabs would otherwise hold a CU to one workgroup).
+Shape pick_shape(const GemmParams& p, bool emu) {
+  const int bm = emu ? 128 : 256;
+  if (p.n <= 32) return {bm, 32};
+  if (p.n <= 64) return {bm, 64};
   return {128, 128};
 }
 
@@ -344,9 +496,8 @@ int64_t pick_splits(const GemmParams& p, Shape sh) {
   return s < 1 ? 1 : s;
 }
 
-template <int BM, int BN, int WM, int WN, bool TA, bool TB, bool EMU>
+template <int BM, int BN, int BK, int WM, int WN, bool TA, bool TB, bool EMU>
 gcn_status launch_tile(const GemmArgs& g, int64_t splits, hipStream_t s) {
-  constexpr int BK = 16;
   dim3 grid((unsigned)ceil_div(g.p.m, BM), (unsigned)ceil_div(g.p.n, BN), (unsigned)splits);
   dim3 block(WM * WN * 64);
   if (splits > 1) {
@@ -366,11 +517,15 @@ gcn_status launch_tile(const GemmArgs& g, int64_t splits, hipStream_t s) {
   return check_launch("gemm");
 }
 
+// Slab depth: 16, except 32 for the plain (NN) bf16x6 product on wide tiles, whose
+// operands both stream from contiguous rows (measured fastest per layout).
 template <bool TA, bool TB, bool EMU>
 gcn_status launch_shape(const GemmArgs& g, Shape sh, int64_t splits, hipStream_t s) {
-  if (sh.bn == 32) return launch_tile<256, 32, 4, 1, TA, TB, EMU>(g, splits, s);
-  if (sh.bn == 64) return launch_tile<256, 64, 4, 1, TA, TB, EMU>(g, splits, s);
-  return launch_tile<128, 128, 2, 2, TA, TB, EMU>(g, splits, s);
+  constexpr int BKW = (EMU && !TA && !TB) ? 32 : 16;
+  constexpr int BMN = EMU ? 128 : 256, WMN = BMN / 64;
+  if (sh.bn == 32) return launch_tile<BMN, 32, 16, WMN, 1, TA, TB, EMU>(g, splits, s);
+  if (sh.bn == 64) return launch_tile<BMN, 64, 16, WMN, 1, TA, TB, EMU>(g, splits, s);
+  return launch_tile<128, 128, BKW, 2, 2, TA, TB, EMU>(g, splits, s);
 }
 
 template <bool TA, bool TB>
@@ -379,22 +534,28 @@ gcn_status launch_layout(const GemmArgs& g, Shape sh, int64_t splits, bool emu, 
 }
 
 // Arithmetic mode: bf16x6 unless GCN_GEMM_MODE=fp32 (native fp32 MFMA, kept for comparison).
-bool use_emulation() {
+// The bf16x6 staging addresses a tile with 32-bit offsets (R * ld * 4 bytes for a
+// k-contiguous operand, R <= 256 rows; 16 * ld * 4 for the other layout); operands with
+// larger pitches take the fp32 mode.
+bool use_emulation(const GemmParams& p) {
   const char* e = getenv("GCN_GEMM_MODE");
-  return !(e && strcmp(e, "fp32") == 0);
+  if (e && strcmp(e, "fp32") == 0) return false;
+  const int64_t lim = (int64_t)1 << 31;
+  return (p.ta ? 16 * p.lda : 256 * p.lda) * 4 < lim && (p.tb ? 256 * p.ldb : 16 * p.ldb) * 4 < lim;
 }
 
 }  // namespace
 
 size_t gemm_workspace(const GemmParams& p) {
-  const Shape sh = pick_shape(p);
+  const Shape sh = pick_shape(p, use_emulation(p));
   const int64_t s = pick_splits(p, sh);
   return s > 1 ? sizeof(float) * (size_t)(s * p.m * p.n) : 0;
 }
 
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   if (p.m == 0 || p.n == 0) return GCN_OK;
-  const Shape sh = pick_shape(p);
+  const bool emu = use_emulation(p);
+  const Shape sh = pick_shape(p, emu);
   const int64_t splits = p.k == 0 ? 1 : pick_splits(p, sh);
   GemmArgs g;
   g.p = p;
@@ -409,7 +570,6 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
            (long)p.m, (long)p.n, (long)p.k);
   ProfScope prof(name, (int32_t)p.n, p.m, p.k, s);
   gcn_status st;
-  const bool emu = use_emulation();
   if (!p.ta && !p.tb) st = launch_layout<false, false>(g, sh, splits, emu, s);
   else if (!p.ta && p.tb) st = launch_layout<false, true>(g, sh, splits, emu, s);
   else if (p.ta && !p.tb) st = launch_layout<true, false>(g, sh, splits, emu, s);

@@ -264,6 +264,20 @@ def test_gemm(G, op, shape):
         assert_mag_close(host(C), ref * (mask > 0), mag, f"gemm {op} mask")
 
 
+def test_gemm_huge_pitch(G):
+    """Operands whose pitch is too large for 32-bit tile offsets (the fp32-mode fallback)."""
+    rng = np.random.default_rng(5)
+    m, n, k, ld = 3, 40, 70, (1 << 21) + 4
+    A = rng.standard_normal((m, k)).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    Ad = pitched(A, ld)
+    C = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    G.gemm(G.OP_NN, Ad, dev(B), C)
+    ref = A.astype(np.float64) @ B.astype(np.float64)
+    mag = np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64))
+    assert_mag_close(host(C), ref, mag, "gemm NN huge pitch")
+
+
 @pytest.mark.parametrize("m,n,k", [(128, 256, 169343), (256, 40, 50000), (100, 256, 70001), (602, 41, 20000),
                                    (4096, 128, 4000), (16, 7, 2708)])
 def test_gemm_tn_long_reduction(G, m, n, k):
