@@ -234,6 +234,11 @@ def main():
         if name.startswith("aggregate_w"):
             by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
             k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+        elif name.startswith("agg_gemm_"):
+            fi, fo = (int(v) for v in name.split("_")[2].split("x"))
+            by = alg_bytes_aggregate(g.nnz, f["rows"], fi) + 4 * f["rows"] * fo
+            k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+            k["TFLOPs"] = round(2 * f["rows"] * fi * fo / (avg * 1e-3) / 1e12, 2)
         elif name.startswith("gemm_"):
             mm, nn, kk = (int(v) for v in name.split("_")[2].split("x"))
             k["TFLOPs"] = round(2 * mm * nn * kk / (avg * 1e-3) / 1e12, 2)

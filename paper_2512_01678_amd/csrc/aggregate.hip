@@ -26,131 +26,14 @@
 // the main kernel skips them; k_chunks sums each GCN_SPLIT_CHUNK-entry chunk
 // into a partial row, and k_combine adds a long row's partials in chunk order
 // and applies the same epilogue.
-#include "internal.h"
+#include "agg_device.h"
 
-#ifndef GCN_AGG_UNR
-#define GCN_AGG_UNR 16  // neighbour-row loads kept in flight per lane, full-wavefront rows
-#endif
+#include <type_traits>
 
 namespace gcn {
 namespace {
 
-template <int VEC>
-struct Vec;
-template <>
-struct Vec<4> {
-  using T = float4;
-  static __device__ __forceinline__ T load(const float* p) { return *reinterpret_cast<const float4*>(p); }
-  static __device__ __forceinline__ void store(float* p, const T& v) { *reinterpret_cast<float4*>(p) = v; }
-  static __device__ __forceinline__ T zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-  static __device__ __forceinline__ void fma(T& acc, float w, const T& x) {
-    acc.x = fmaf(w, x.x, acc.x);
-    acc.y = fmaf(w, x.y, acc.y);
-    acc.z = fmaf(w, x.z, acc.z);
-    acc.w = fmaf(w, x.w, acc.w);
-  }
-  static __device__ __forceinline__ void add(T& acc, const T& x) {
-    acc.x += x.x;
-    acc.y += x.y;
-    acc.z += x.z;
-    acc.w += x.w;
-  }
-  static __device__ __forceinline__ float get(const T& v, int i) {
-    return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
-  }
-  static __device__ __forceinline__ void add_xor(T& v, int o, int width) {
-    v.x += __shfl_xor(v.x, o, width);
-    v.y += __shfl_xor(v.y, o, width);
-    v.z += __shfl_xor(v.z, o, width);
-    v.w += __shfl_xor(v.w, o, width);
-  }
-};
-template <>
-struct Vec<1> {
-  using T = float;
-  static __device__ __forceinline__ T load(const float* p) { return *p; }
-  static __device__ __forceinline__ void store(float* p, const T& v) { *p = v; }
-  static __device__ __forceinline__ T zero() { return 0.f; }
-  static __device__ __forceinline__ void fma(T& acc, float w, const T& x) { acc = fmaf(w, x, acc); }
-  static __device__ __forceinline__ void add(T& acc, const T& x) { acc += x; }
-  static __device__ __forceinline__ float get(const T& v, int) { return v; }
-  static __device__ __forceinline__ void add_xor(T& v, int o, int width) { v += __shfl_xor(v, o, width); }
-};
-
-template <int LANES>
-__device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int o = LANES / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, LANES));
-  return v;
-}
-template <int LANES>
-__device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int o = LANES / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, LANES);
-  return v;
-}
-
 constexpr int kBlock = 256;
-
-// Lane geometry of a group of LANES * slots lanes owning one (virtual) row.
-struct Lanes {
-  int gw, lig, slot, lane, c0;
-};
-
-template <int LANES, int VEC>
-__device__ __forceinline__ Lanes lanes_of(int slots) {
-  Lanes L;
-  L.gw = LANES * slots;
-  L.lig = threadIdx.x & (L.gw - 1);
-  L.slot = L.lig / LANES;
-  L.lane = L.lig & (LANES - 1);
-  L.c0 = (blockIdx.y * LANES + L.lane) * VEC;
-  return L;
-}
-
-// sum_{e in [beg, end)} w_e M[col[e], c0 .. c0+VEC), every slice of the group holding the
-// total.  first_j: the group's column indices of the first gw entries (lane lig holds
-// entry beg + lig), already loaded by the caller.
-template <int LANES, int VEC>
-__device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, int64_t beg, int64_t end,
-                                                           const Lanes& L, int slots, bool cok, int first_j) {
-  using V = Vec<VEC>;
-  constexpr int UNR = LANES == 64 ? GCN_AGG_UNR : (LANES >= 4 ? 8 : 4);
-  typename V::T acc = V::zero();
-  const float* Mc = p.M + L.c0;
-  for (int64_t base = beg; base < end; base += L.gw) {
-    const int cnt = (int)((end - base) < L.gw ? (end - base) : L.gw);
-    int my_j = first_j;
-    if (base != beg) my_j = L.lig < cnt ? p.col[base + L.lig] : 0;
-    float my_w = 0.f;
-    if (L.lig < cnt) my_w = p.val[base + L.lig];
-    for (int t = 0; t < cnt; t += slots * UNR) {
-      int jj[UNR];
-      float ww[UNR];
-      bool ok[UNR];
-      typename V::T xs[UNR];
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const int e = t + u * slots + L.slot;
-        ok[u] = e < cnt;
-        jj[u] = __shfl(my_j, ok[u] ? e : 0, L.gw);
-      }
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) xs[u] = (ok[u] && cok) ? V::load(Mc + (int64_t)jj[u] * p.ldm) : V::zero();
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) ww[u] = __shfl(my_w, ok[u] ? t + u * slots + L.slot : 0, L.gw);
-#pragma unroll
-      for (int u = 0; u < UNR; ++u) V::fma(acc, ok[u] ? ww[u] : 0.f, xs[u]);
-    }
-  }
-  for (int o = LANES; o < L.gw; o <<= 1) V::add_xor(acc, o, L.gw);
-  return acc;
-}
-
-template <int LANES>
-__device__ __forceinline__ int load_first_chunk(const AggParams& p, int64_t beg, int64_t end, const Lanes& L) {
-  return (beg + L.lig < end) ? p.col[beg + L.lig] : 0;
-}
 
 // Bias and epilogue of one row; slice 0 writes.
 template <int LANES, int VEC, int EPI>
@@ -241,7 +124,7 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, in
   const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
   if (end - beg > skip_over) return;
   const bool cok = L.c0 < p.w;
-  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
+  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
   finish_row<LANES, VEC, EPI>(p, row, acc, L, cok);
 }
 
@@ -258,7 +141,7 @@ __global__ void __launch_bounds__(kBlock) k_chunks(AggParams p, gcn_split sp, in
   const int64_t rend = p.row_ptr[row + 1];
   const int64_t end = beg + GCN_SPLIT_CHUNK < rend ? beg + GCN_SPLIT_CHUNK : rend;
   const bool cok = L.c0 < p.w;
-  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first_chunk<LANES>(p, beg, end, L));
+  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
   if (cok && L.slot == 0) Vec<VEC>::store(part + ch * pw + L.c0, acc);
 }
 
@@ -359,6 +242,39 @@ bool use_vec4(const AggParams& p) {
 }
 
 }  // namespace
+
+gcn_status launch_aggregate_long_rows(const AggParams& p, const gcn_split* split, void* ws, hipStream_t s) {
+  if (!has_split(split) || p.w == 0) return GCN_OK;
+  if (!use_vec4(p) || p.epi != AGG_NONE)
+    return fail(GCN_E_UNSUPPORTED, "long-row aggregation: needs 16-byte rows and no epilogue");
+  int lanes = 1;
+  while (lanes < ceil_div(p.w, 4) && lanes < 64) lanes <<= 1;
+  const int slots = std::min(64 / lanes, 16);
+  const int gw = lanes * slots;
+  const unsigned gy = (unsigned)ceil_div(p.w, lanes * 4);
+  const int64_t pw = round_up(p.w, 4);
+  float* part = static_cast<float*>(ws);
+  auto run = [&](auto tag) -> gcn_status {
+    constexpr int LN = decltype(tag)::value;
+    hipLaunchKernelGGL((k_chunks<LN, 4>), dim3((unsigned)ceil_div(split->n_chunk, kBlock / gw), gy), dim3(kBlock),
+                       0, s, p, *split, slots, part, pw);
+    GCN_TRY(check_launch("aggregate chunks"));
+    hipLaunchKernelGGL((k_combine<LN, 4, AGG_NONE>), dim3((unsigned)ceil_div(split->n_long, kBlock / LN), gy),
+                       dim3(kBlock), 0, s, p, *split, 1, part, pw);
+    return check_launch("aggregate combine");
+  };
+  switch (lanes) {
+    case 1: return run(std::integral_constant<int, 1>{});
+    case 2: return run(std::integral_constant<int, 2>{});
+    case 4: return run(std::integral_constant<int, 4>{});
+    case 8: return run(std::integral_constant<int, 8>{});
+    case 16: return run(std::integral_constant<int, 16>{});
+    case 32: return run(std::integral_constant<int, 32>{});
+    default: return run(std::integral_constant<int, 64>{});
+  }
+}
+
+int agg_slots(int lanes, int64_t nnz, int64_t rows) { return pick_slots(lanes, nnz, rows); }
 
 size_t aggregate_workspace(const gcn_split* split, int32_t w) {
   if (!has_split(split)) return 0;

@@ -86,6 +86,14 @@ int32_t resolve_order(const gcn_layer* L, bool x_sparse) {
   return af < 2 * (int64_t)L->f_out ? GCN_AGGREGATE_FIRST : GCN_TRANSFORM_FIRST;
 }
 
+// The fused aggregate-first kernel serves 32 < f_in <= 128 in bf16x6 mode;
+// GCN_AF_FUSED=0 selects the two-launch form (kept for comparison).
+bool af_fusable(int32_t f_in) {
+  const char* e = getenv("GCN_AF_FUSED");
+  if (e && e[0] == '0') return false;
+  return gemm_bf16x6_mode() && f_in > 32 && f_in <= 128;
+}
+
 AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, float* Z, int64_t ldz) {
   AggParams p{};
   p.n = g->n;
@@ -130,15 +138,25 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
   if (order == GCN_AGGREGATE_FIRST) {
-    // P = A_hat H_in (kept for the backward pass), then H_out = act(P W + b)
-    void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_in));
+    // P = A_hat H_in (kept for the backward pass), then H_out = act(P W + b): one fused
+    // kernel when the widths allow it (bf16x6 mode), else an aggregation and a GEMM.
+    // The workspace covers both, so a size query made without buffers stays valid.
+    const bool fusable = af_fusable(L->f_in);
+    size_t need = aggregate_workspace(&g->split, L->f_in);
+    if (fusable) need = std::max(need, agg_gemm_workspace(&g->split, L->f_in, L->f_out));
+    void* aws = a.take<char>((int64_t)need);
     if (run) {
       AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in);
-      GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
-      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
-      q.bias = b;
-      q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
-      GCN_TRY(launch_gemm(q, nullptr, s));
+      if (fusable && agg_gemm_supported(L->f_in, L->ld_in, L->ld_in, Hin, saved)) {
+        GCN_TRY(launch_agg_gemm(p, g->nnz, &g->split, W, L->f_out, L->f_out, b, L->act == GCN_ACT_RELU, Hout,
+                                L->ld_out, aws, s));
+      } else {
+        GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
+        GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
+        q.bias = b;
+        q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
+        GCN_TRY(launch_gemm(q, nullptr, s));
+      }
     }
     return GCN_OK;
   }

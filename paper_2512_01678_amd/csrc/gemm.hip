@@ -32,13 +32,11 @@
 //    product on gfx950), and every fragment is one 16-byte LDS read.
 #include <cstring>
 
-#include "internal.h"
+#include "bf16x6.h"
 
 namespace gcn {
 namespace {
 
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kPad = 4;
 
@@ -124,22 +122,6 @@ struct Stage {
     return KCONT ? lds[rr * (BK + kPad) + kidx] : lds[kidx * (R + kPad) + rr];
   }
 };
-
-// Two round-to-nearest bf16 values packed in one dword (a in the low half).
-__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
-  typedef float f2 __attribute__((ext_vector_type(2)));
-  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
-  const f2 v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2));
-}
-
-// Exact three-way split of a pair: a = hi + mid + lo (each part a bf16), packed per part.
-__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
-  hi = pk_bf16(a, b);
-  const float ra = a - __uint_as_float(hi << 16), rb = b - __uint_as_float(hi & 0xffff0000u);
-  mid = pk_bf16(ra, rb);
-  lo = pk_bf16(ra - __uint_as_float(mid << 16), rb - __uint_as_float(mid & 0xffff0000u));
-}
 
 // Staging of one operand slab for the bf16x6 mode: every element is split once, when
 // the slab goes into LDS, into three bf16 planes laid out k-contiguous,
@@ -538,13 +520,17 @@ gcn_status launch_layout(const GemmArgs& g, Shape sh, int64_t splits, bool emu, 
 // k-contiguous operand, R <= 256 rows; 16 * ld * 4 for the other layout); operands with
 // larger pitches take the fp32 mode.
 bool use_emulation(const GemmParams& p) {
-  const char* e = getenv("GCN_GEMM_MODE");
-  if (e && strcmp(e, "fp32") == 0) return false;
+  if (!gemm_bf16x6_mode()) return false;
   const int64_t lim = (int64_t)1 << 31;
   return (p.ta ? 16 * p.lda : 256 * p.lda) * 4 < lim && (p.tb ? 256 * p.ldb : 16 * p.ldb) * 4 < lim;
 }
 
 }  // namespace
+
+bool gemm_bf16x6_mode() {
+  const char* e = getenv("GCN_GEMM_MODE");
+  return !(e && strcmp(e, "fp32") == 0);
+}
 
 size_t gemm_workspace(const GemmParams& p) {
   const Shape sh = pick_shape(p, use_emulation(p));

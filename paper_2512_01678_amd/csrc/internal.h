@@ -96,6 +96,19 @@ size_t aggregate_workspace(const gcn_split* split, int32_t w);
 gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* split, void* ws,
                             hipStream_t s);
 inline bool has_split(const gcn_split* sp) { return sp && sp->rows && sp->n_long > 0; }
+// Neighbour slices per row for slices of `lanes` lanes on a matrix with nnz entries over
+// `rows` rows (nnz < 0: unknown).
+int agg_slots(int lanes, int64_t nnz, int64_t rows);
+// Only the long rows of a split plan (chunk sums, then their combination), no epilogue.
+gcn_status launch_aggregate_long_rows(const AggParams& p, const gcn_split* split, void* ws, hipStream_t s);
+
+// Aggregate-first layer in one kernel: P = A_hat X (written to a.Z), H = act(P W + b),
+// in the bf16x6 arithmetic of the dense products.  W is f_in x f_out (pitch ldw).
+bool agg_gemm_supported(int32_t f_in, int64_t ldx, int64_t ldp, const float* X, const float* P);
+size_t agg_gemm_workspace(const gcn_split* split, int32_t f_in, int32_t f_out);
+gcn_status launch_agg_gemm(const AggParams& a, int64_t nnz, const gcn_split* split, const float* W,
+                           int64_t ldw, int32_t f_out, const float* bias, bool relu, float* H, int64_t ldh,
+                           void* ws, hipStream_t s);
 
 // split plan of the long rows of a compressed matrix with offsets ptr[0..nrows]
 size_t split_workspace(int64_t nrows);
@@ -121,6 +134,8 @@ struct GemmParams {
   int64_t ldmask;
 };
 size_t gemm_workspace(const GemmParams& p);
+// Arithmetic of the dense products: bf16x6 (default) unless GCN_GEMM_MODE=fp32.
+bool gemm_bf16x6_mode();
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s);
 
 size_t colsum_workspace(int64_t rows, int32_t w);

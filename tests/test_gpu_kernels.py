@@ -411,6 +411,26 @@ def test_softmax_layer_on_split_hubs(G, orc, hub_graph):
     np.testing.assert_allclose(host(out), Gr, rtol=0, atol=1e-4 * np.abs(Gr).max())
 
 
+@pytest.mark.parametrize("fi,fo", [(128, 256), (48, 300)])
+def test_aggregate_first_layer_on_split_hubs(G, orc, hub_graph, fi, fo):
+    """Fused aggregate-then-transform layer: hub rows come from the chunk kernels."""
+    og, dg = hub_graph
+    n = og.n
+    rng = np.random.default_rng(fi)
+    H = rng.standard_normal((n, fi)).astype(np.float32)
+    W = (rng.standard_normal((fi, fo)) / np.sqrt(fi)).astype(np.float32)
+    b = (rng.standard_normal(fo) * 0.1).astype(np.float32)
+    L = G.make_layer(fi, fo, G.pitch(fi), G.pitch(fo), G.ACT_RELU, 0, G.AGGREGATE_FIRST)
+    out = pitched(np.zeros((n, fo), np.float32), G.pitch(fo))
+    saved = pitched(np.zeros((n, fi), np.float32), G.pitch(fi))
+    G.layer_fwd(dg, L, pitched(H, G.pitch(fi)), None, dev(W), dev(b), out, saved=saved)
+    P, pmag = orc.aggregate(og, H, want_mag=True)
+    assert_mag_close(host(saved), P, pmag, "split hubs: saved A_hat H")
+    Z = orc.aggregate(og, orc.matmul(H, W), b)
+    mag = orc.aggregate(og, orc.matmul(np.abs(H), np.abs(W)), np.abs(b))
+    assert_mag_close(host(out), np.maximum(Z, 0), mag, f"split hubs: AF {fi}->{fo}")
+
+
 def test_sparse_backward_long_columns(G, orc):
     """X with few, dense columns: every CSC column is long and goes through chunks
     processed chunk-index-major."""

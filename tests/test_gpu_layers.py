@@ -70,7 +70,8 @@ def abs_agg(orc, og, A):
 
 @pytest.mark.parametrize("order", ["TF", "AF"])
 @pytest.mark.parametrize("fi,fo,act", [(128, 256, "relu"), (256, 40, "softmax"), (100, 256, "relu"),
-                                       (41, 47, "none"), (256, 7, "softmax"), (602, 256, "relu")])
+                                       (41, 47, "none"), (256, 7, "softmax"), (602, 256, "relu"),
+                                       (64, 300, "relu"), (33, 5, "none"), (120, 520, "relu")])
 def test_layer_forward(G, orc, small, order, fi, fo, act):
     if order == "AF" and act == "softmax":
         pytest.skip("aggregate-first is never chosen for the loss layer")
@@ -103,6 +104,28 @@ def test_layer_forward(G, orc, small, order, fi, fo, act):
     if order == "AF":
         P, pmag = orc.aggregate(og, H, want_mag=True)
         assert_mag_close(host(saved), P, pmag, "saved A_hat H")
+
+
+@pytest.mark.parametrize("fi,fo", [(128, 256), (100, 256), (41, 47), (64, 300)])
+def test_aggregate_first_fused_matches_two_launches(G, small, fi, fo, monkeypatch):
+    """The fused aggregate-then-transform kernel against the aggregation + GEMM pair:
+    the saved aggregate is bit-identical (same accumulation code), the output agrees
+    to fp32 rounding (same bf16x6 arithmetic, different grouping of k)."""
+    dg, n = small.dg, small.wl.n
+    rng = np.random.default_rng(fi * fo)
+    H = rng.standard_normal((n, fi)).astype(np.float32)
+    W = (rng.standard_normal((fi, fo)) / np.sqrt(fi)).astype(np.float32)
+    b = (rng.standard_normal(fo) * 0.1).astype(np.float32)
+    L = G.make_layer(fi, fo, G.pitch(fi), G.pitch(fo), G.ACT_RELU, 0, G.AGGREGATE_FIRST)
+    res = {}
+    for mode in ("1", "0"):
+        monkeypatch.setenv("GCN_AF_FUSED", mode)
+        out, saved = G.padded(n, fo), G.padded(n, fi)
+        G.layer_fwd(dg, L, pad(G, H), None, dev(W), dev(b), out, saved=saved)
+        res[mode] = (host(out), host(saved))
+    np.testing.assert_array_equal(res["1"][1], res["0"][1])
+    scale = np.abs(res["0"][0]).max()
+    assert np.abs(res["1"][0] - res["0"][0]).max() <= 1e-5 * scale
 
 
 @pytest.mark.parametrize("order", ["TF", "AF"])
