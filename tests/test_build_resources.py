@@ -56,6 +56,6 @@ def test_no_kernel_uses_scratch(tmp_path):
     meta = kernel_metadata(G.LIB_PATH, str(tmp_path))
     assert len(meta) >= 40, sorted(meta)
     assert any("k_aggregate" in k for k in meta) and any("k_gemm" in k for k in meta)
-    bad = {k: v for k, v in meta.items() if v.get("private_segment_fixed_size", 0) or v.get("vgpr_spill_count", 0)
-           or v.get("sgpr_spill_count", 0)}
+    # scalar-register spills land in vector-register lanes, not memory, and are allowed
+    bad = {k: v for k, v in meta.items() if v.get("private_segment_fixed_size", 0) or v.get("vgpr_spill_count", 0)}
     assert not bad, bad
