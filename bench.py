@@ -61,8 +61,8 @@ def sha_of(path):
 
 
 def traffic_for(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if the kernel
-    source is unchanged since the counters were taken; else None."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if the kernel's
+    source files are unchanged since the counters were taken; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -71,12 +71,13 @@ def traffic_for(kernel: str, workload: str):
     except (OSError, ValueError):
         return None
     rec = table.get(f"{kernel}@{workload}")
-    if not rec:
+    if not isinstance(rec, dict) or not isinstance(rec.get("sources"), dict) or not rec["sources"]:
         return None
-    src = os.path.join(ROOT, rec["source"])
-    if not os.path.exists(src) or sha_of(src) != rec["source_sha256"]:
-        return None
-    return rec["bytes_per_launch"]
+    for rel, sha in rec["sources"].items():
+        src = os.path.join(ROOT, rel)
+        if not os.path.exists(src) or sha_of(src) != sha:
+            return None
+    return rec.get("bytes_per_launch")
 
 
 def copy_calibration(gib: float):
@@ -127,8 +128,9 @@ def cpu_baseline(wl, s, d, X, y, Ws, bs, sparse: bool, budget_s: float):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the multi-GPU path "
-              "is not built -- see DESIGN.md for how it would shard", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the multi-GPU form "
+              "(one process per GPU over a row partition of A_hat, halo rows exchanged over RCCL) "
+              "is not built", file=sys.stderr)
         sys.exit(2)
     import torch
     if args.copy_gib > 0:
