@@ -470,9 +470,11 @@ Shape pick_shape(const GemmParams& p, bool emu) {
 
 int64_t pick_splits(const GemmParams& p, Shape sh) {
   if (!p.ta) return 1;  // only A^T B reduces over the long (row) dimension
-  // about 1024 workgroups, each walking at least 256 rows of k
+  // about 2048 wavefronts in all (measured best for wide and narrow tiles alike), each
+  // workgroup walking at least 256 rows of k
   const int64_t tiles = ceil_div(p.m, sh.bm) * ceil_div(p.n, sh.bn);
-  int64_t s = ceil_div(1024, tiles);
+  const int64_t waves = sh.bn >= 128 ? 4 : sh.bm / 64;
+  int64_t s = ceil_div(2048, tiles * waves);
   const int64_t max_s = ceil_div(p.k, 256);
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;
@@ -632,25 +634,30 @@ __global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w,
   }
 }
 
-// out[c] = sum_b part[b][c]: 8 columns per workgroup, 32 lanes per column; lane q
-// sums b = q, q + 32, ... in increasing order, then the 32 lane sums are combined by
-// a fixed binary tree.
+// out[c] = sum_b part[b][c]: 4 columns per workgroup, one wavefront per column; lane q
+// sums b = q, q + 64, ... in increasing order into 4 interleaved accumulators (combined
+// in order), then the 64 lane sums are combined by a fixed binary tree.
 __global__ void __launch_bounds__(256) k_colsum_final(const double* part, int nblk, int32_t w, int32_t pw,
                                                       float* out, float* mean, double inv_rows) {
-  __shared__ double red[32][8];
-  const int cl = threadIdx.x % 8, q = threadIdx.x / 8;
-  const int col = blockIdx.x * 8 + cl;
-  double s = 0.0;
-  if (col < pw)
-    for (int b = q; b < nblk; b += 32) s += part[(int64_t)b * pw + col];
-  red[q][cl] = s;
+  __shared__ double red[4][64];
+  const int q = threadIdx.x % 64, cl = threadIdx.x / 64;
+  const int col = blockIdx.x * 4 + cl;
+  double a[4] = {0.0, 0.0, 0.0, 0.0};
+  if (col < pw) {
+    int b = q;
+    for (; b + 192 < nblk; b += 256)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] += part[(int64_t)(b + 64 * u) * pw + col];
+    for (; b < nblk; b += 64) a[0] += part[(int64_t)b * pw + col];
+  }
+  red[cl][q] = (a[0] + a[1]) + (a[2] + a[3]);
   __syncthreads();
-  for (int o = 16; o > 0; o >>= 1) {
-    if (q < o) red[q][cl] += red[q + o][cl];
+  for (int o = 32; o > 0; o >>= 1) {
+    if (q < o) red[cl][q] += red[cl][q + o];
     __syncthreads();
   }
   if (q == 0 && col < pw) {
-    const double t = red[0][cl];
+    const double t = red[cl][0];
     if (col < w) out[col] = (float)t;
     else if (mean) *mean = (float)(t * inv_rows);
   }
@@ -672,7 +679,7 @@ gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, f
   hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
                      part, pw, vec);
   GCN_TRY(check_launch("column sums"));
-  hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 8)), dim3(256), 0, s, part, nblk, w, pw,
+  hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 4)), dim3(256), 0, s, part, nblk, w, pw,
                      out, mean, rows > 0 ? 1.0 / (double)rows : 0.0);
   return check_launch("column sums final");
 }
