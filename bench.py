@@ -258,6 +258,26 @@ def main():
                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(name, wl.name),
                     "kernel": name, "alg_bytes_per_launch": by, "avg_launch_ms": round(avg_s * 1e3, 5)}
 
+    # every aggregation launch: bytes-weighted achieved rate of the graph SpMM
+    spmm = None
+    agg_fams = [(f, alg_bytes_aggregate(g.nnz, f["rows"], f["width"])) for k, f in fam.items()
+                if k.startswith("aggregate_w")]
+    if agg_fams:
+        tot_b = sum(by * f["count"] for f, by in agg_fams)
+        tot_s = sum(f["ms"] for f, _ in agg_fams) * 1e-3
+        spmm = {"weighted_GBps": round(tot_b / tot_s / 1e9, 1),
+                "frac": round(tot_b / tot_s / 1e9 / HBM_PEAK_GBS, 4),
+                "launches_per_epoch": sum(f["count"] for f, _ in agg_fams) // args.steps}
+
+    # device memory: allocator high-water mark against the O(N F) model (no O(nnz F) term)
+    graph_bytes = 8 * (wl.n + 1) + 8 * g.col_idx.numel() + 8 * wl.n  # offsets, indices + values, deg + dinv
+    x_bytes = 0 if sparse else 4 * wl.n * ld_x
+    act_floats = sum(G.pitch(w) for w in wl.widths[1:]) + (G.pitch(wl.widths[1]) if not sparse else 0)
+    peak = torch.cuda.max_memory_allocated(dev)
+    memory = {"peak_bytes": peak, "graph_bytes": graph_bytes, "x_bytes": x_bytes,
+              "rest_floats_per_node": round((peak - graph_bytes - x_bytes) / (4 * wl.n), 1),
+              "activation_floats_per_node": act_floats}
+
     cpu = None
     if args.cpu_baseline == "auto" and X is None:
         print("[bench] no host copy of X for this workload: cpu_baseline skipped", file=sys.stderr, flush=True)
@@ -276,7 +296,7 @@ def main():
                    "per_launch_events": profile, "hip_graph": bool(args.graph),
                    "gemm_mode": "fp32 MFMA" if os.environ.get("GCN_GEMM_MODE") == "fp32"
                    else "fp32 via exact 3-way bf16 split, 6 bf16 MFMA products"},
-        "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
+        "roofline": roofline, "cpu_baseline": cpu, "spmm": spmm, "memory": memory, "kernels": kernels,
         "setup_ms": {"csr_build": round(t_csr * 1e3, 2), "density_probe": round(t_probe * 1e3, 2)},
     }
     print(json.dumps(out))

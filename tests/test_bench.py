@@ -61,3 +61,12 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120, env={**os.environ, "HIP_VISIBLE_DEVICES": ""})
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr)
+
+
+def test_calibration_crossover_interpolation():
+    import calibrate
+    # ratio t_sparse / t_dense crosses 1 between densities 0.01 and 0.1, at the geometric mean
+    # when the two ratios are symmetric about 1
+    c = calibrate.crossover([(0.1, 1.5), (0.01, 0.5), (0.5, 4.0)])
+    assert c == pytest.approx((0.01 * 0.1) ** 0.5, rel=1e-12)
+    assert calibrate.crossover([(0.1, 0.5), (0.5, 0.9)]) is None  # sparse faster everywhere
