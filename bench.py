@@ -182,6 +182,8 @@ def main():
     if sparse:
         del Xv, Xd  # the sparse path reads only X_csr / X_csc
         torch.cuda.empty_cache()
+    setup_peak = torch.cuda.max_memory_allocated(dev)
+    torch.cuda.reset_peak_memory_stats(dev)
     m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x, device_step=args.graph)
     Xin = None if sparse else Xv
     for _ in range(args.warmup):
@@ -269,14 +271,17 @@ def main():
                 "frac": round(tot_b / tot_s / 1e9 / HBM_PEAK_GBS, 4),
                 "launches_per_epoch": sum(f["count"] for f, _ in agg_fams) // args.steps}
 
-    # device memory: allocator high-water mark against the O(N F) model (no O(nnz F) term)
+    # device memory during training (allocator high-water mark from the model's creation
+    # on) against the O(N F) model: nothing may scale with nnz times a feature width
     graph_bytes = 8 * (wl.n + 1) + 8 * g.col_idx.numel() + 8 * wl.n  # offsets, indices + values, deg + dinv
     x_bytes = 0 if sparse else 4 * wl.n * ld_x
-    act_floats = sum(G.pitch(w) for w in wl.widths[1:]) + (G.pitch(wl.widths[1]) if not sparse else 0)
-    peak = torch.cuda.max_memory_allocated(dev)
-    memory = {"peak_bytes": peak, "graph_bytes": graph_bytes, "x_bytes": x_bytes,
-              "rest_floats_per_node": round((peak - graph_bytes - x_bytes) / (4 * wl.n), 1),
-              "activation_floats_per_node": act_floats}
+    if sparse:  # X_csr and X_csc: offsets, indices, values
+        x_bytes = 8 * (wl.n + 1) + 8 * (wl.f + 1) + 16 * sx.col.numel()
+    train_peak = torch.cuda.max_memory_allocated(dev)
+    memory = {"train_peak_bytes": train_peak, "setup_peak_bytes": setup_peak, "graph_bytes": graph_bytes,
+              "x_bytes": x_bytes,
+              "other_floats_per_node": round((train_peak - graph_bytes - x_bytes) / (4 * wl.n), 1),
+              "layer_output_floats_per_node": sum(G.pitch(w) for w in wl.widths[1:])}
 
     cpu = None
     if args.cpu_baseline == "auto" and X is None:
