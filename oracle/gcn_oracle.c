@@ -150,17 +150,30 @@ void orc_dense_to_csc(const float* X, int32_t n, int32_t f, int64_t ldx, int64_t
 }
 
 /*
- * Normalised aggregation Z = A_hat M + 1 b^T with A_hat = D^-1/2 (A + I) D^-1/2
- * (Section III-A; Algorithm 3 computes Y[u] = sum_e val[e] X[col[e]] over the
- * CSR row of u, here with val = 1 / sqrt(d_u d_v)).
+ * Linear aggregation Z = S M + 1 b^T over the rows of A + I (Section III-A, the
+ * AGGREGATE step of a GNN layer; Algorithm 3 computes Y[u] = sum_e val[e] X[col[e]]
+ * over the CSR row of u).  The operator S by `kind`:
+ *   0  GCN normalised mean aggregation: S_uv = 1 / sqrt(d_u d_v)  (D^-1/2 (A+I) D^-1/2)
+ *   1  sum aggregation (GIN with epsilon = 0): S_uv = 1             (A + I)
+ *   2  mean aggregation: S_uv = 1 / d_u                             (D^-1 (A + I))
+ *   3  transpose of the mean: S_uv = 1 / d_v                        ((A + I) D^-1)
  *
  * Rows listed in `rows` (all rows when rows == NULL) are written to Z at row
  * index r (the listed position when rows != NULL).  mag, when non-NULL, gets
- * sum |A_hat_uv| |M_vc| + |b_c|, the magnitude scale of each output element.
+ * sum |S_uv| |M_vc| + |b_c|, the magnitude scale of each output element.
  */
+static double orc_weight(int32_t kind, int32_t du, int32_t dv) {
+  switch (kind) {
+    case 1: return 1.0;
+    case 2: return 1.0 / (double)du;
+    case 3: return 1.0 / (double)dv;
+    default: return 1.0 / sqrt((double)du * (double)dv);
+  }
+}
+
 void orc_aggregate(int32_t n, const int64_t* row_ptr, const int32_t* col_idx, const int32_t* deg,
                    const double* M, int64_t ldm, int32_t w, const double* bias, double* Z,
-                   int64_t ldz, double* mag, const int32_t* rows, int64_t nrows) {
+                   int64_t ldz, double* mag, const int32_t* rows, int64_t nrows, int32_t kind) {
   int64_t count = rows ? nrows : n;
 #pragma omp parallel for schedule(dynamic, 64)
   for (int64_t r = 0; r < count; ++r) {
@@ -173,7 +186,7 @@ void orc_aggregate(int32_t n, const int64_t* row_ptr, const int32_t* col_idx, co
     }
     for (int64_t e = row_ptr[u]; e < row_ptr[u + 1]; ++e) {
       int32_t v = col_idx[e];
-      double a = 1.0 / sqrt((double)deg[u] * (double)deg[v]);
+      double a = orc_weight(kind, deg[u], deg[v]);
       const double* mv = M + (int64_t)v * ldm;
       for (int32_t c = 0; c < w; ++c) {
         z[c] += a * mv[c];
@@ -212,4 +225,43 @@ void orc_spmm(int64_t nrows, const int64_t* ptr, const int32_t* idx, const doubl
       }
     }
   }
+}
+
+/*
+ * Max aggregation (the "Max" aggregator of Listing 1; Section III-A lists mean,
+ * max and sum): P[u,c] = max over the row of A + I of M[v,c], and argmax[u,c] =
+ * the first v (columns ascending) that attains it.
+ */
+void orc_aggregate_max(int32_t n, const int64_t* row_ptr, const int32_t* col_idx, const double* M,
+                       int64_t ldm, int32_t w, double* P, int32_t* argmax) {
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int32_t u = 0; u < n; ++u) {
+    for (int32_t c = 0; c < w; ++c) {
+      double best = 0.0;
+      int32_t arg = -1;
+      for (int64_t e = row_ptr[u]; e < row_ptr[u + 1]; ++e) {
+        int32_t v = col_idx[e];
+        double x = M[(int64_t)v * ldm + c];
+        if (arg < 0 || x > best) {
+          best = x;
+          arg = v;
+        }
+      }
+      P[(int64_t)u * w + c] = best;
+      argmax[(int64_t)u * w + c] = arg;
+    }
+  }
+}
+
+/*
+ * Gradient of the max aggregation: each output element passes its gradient to the
+ * one input it copied, dM[argmax[u,c], c] += dP[u,c] (every other input gets 0).
+ * Written as that scatter, in row order, on one thread.
+ */
+void orc_aggregate_max_backward(int32_t n, const double* dP, int32_t w, const int32_t* argmax,
+                                double* dM, int64_t ldo) {
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t c = 0; c < w; ++c) dM[(int64_t)u * ldo + c] = 0.0;
+  for (int32_t u = 0; u < n; ++u)
+    for (int32_t c = 0; c < w; ++c) dM[(int64_t)argmax[(int64_t)u * w + c] * ldo + c] += dP[(int64_t)u * w + c];
 }

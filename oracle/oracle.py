@@ -9,7 +9,8 @@ computes (paper: "Morphling: Fast, Fused, and Flexible GNN Training at
 Scale", arXiv 2512.01678):
 
 * the graph operator A_hat = D^-1/2 (A + I) D^-1/2 in CSR form (Section III-A,
-  GCN "normalized mean aggregation"),
+  GCN "normalized mean aggregation"), and the other aggregators Section III-A and
+  Listing 1 name: sum (A + I), mean (D^-1 (A + I)) and max (with its argmax),
 * the density probe and the dense/sparse decision s >= tau (Section IV-B,
   Algorithm 1, Initialize), with DenseToCSR / DenseToCSC,
 * the forward pass Z_l = A_hat (H_l W_l) + b_l, H_{l+1} = ReLU(Z_l) (the
@@ -74,7 +75,11 @@ def lib():
         L.orc_dense_to_csc.restype = None
         L.orc_dense_to_csc.argtypes = [P, i32, i32, i64, P, P, P]
         L.orc_aggregate.restype = None
-        L.orc_aggregate.argtypes = [i32, P, P, P, P, i64, i32, P, P, i64, P, P, i64]
+        L.orc_aggregate.argtypes = [i32, P, P, P, P, i64, i32, P, P, i64, P, P, i64, i32]
+        L.orc_aggregate_max.restype = None
+        L.orc_aggregate_max.argtypes = [i32, P, P, P, i64, i32, P, P]
+        L.orc_aggregate_max_backward.restype = None
+        L.orc_aggregate_max_backward.argtypes = [i32, P, i32, P, P, i64]
         L.orc_spmm.restype = None
         L.orc_spmm.argtypes = [i64, P, P, P, P, i64, i32, P, i64, P]
         _lib = L
@@ -172,10 +177,18 @@ def dense_to_csc(X: np.ndarray):
 # ---------------------------------------------------------------------------
 
 
-def aggregate(g: Graph, M: np.ndarray, bias=None, rows=None, want_mag: bool = False):
-    """Z = A_hat M + 1 b^T on all rows, or on the listed rows (Section III-A, Algorithm 3).
+# linear aggregators (the AGGREGATE step of Section III-A): operator over the rows of A + I
+KINDS = {"gcn": 0, "sum": 1, "mean": 2, "mean_t": 3}
+# the operator that carries gradients back through each one (A_hat and A + I are symmetric)
+TRANSPOSE = {"gcn": "gcn", "sum": "sum", "mean": "mean_t", "mean_t": "mean"}
 
-    Returns Z (and the magnitude scale sum |A_hat||M| + |b| when want_mag).
+
+def aggregate(g: Graph, M: np.ndarray, bias=None, rows=None, want_mag: bool = False, kind: str = "gcn"):
+    """Z = S M + 1 b^T on all rows, or on the listed rows (Section III-A, Algorithm 3).
+
+    S = A_hat = D^-1/2 (A+I) D^-1/2 ("gcn"), A + I ("sum"), D^-1 (A+I) ("mean") or
+    (A+I) D^-1 ("mean_t", the transpose of the mean).  Returns Z (and the magnitude
+    scale sum |S||M| + |b| when want_mag).
     """
     M = np.ascontiguousarray(M, np.float64)
     w = M.shape[1]
@@ -186,8 +199,33 @@ def aggregate(g: Graph, M: np.ndarray, bias=None, rows=None, want_mag: bool = Fa
     mag = np.zeros((cnt, w), np.float64) if want_mag else None
     if w > 0 and cnt > 0:
         lib().orc_aggregate(g.n, _p(g.row_ptr), _p(g.col_idx), _p(g.deg), _p(M), w, w, _p(b),
-                            _p(Z), w, _p(mag), _p(r), cnt)
+                            _p(Z), w, _p(mag), _p(r), cnt, KINDS[kind])
     return (Z, mag) if want_mag else Z
+
+
+def aggregate_max(g: Graph, M: np.ndarray):
+    """Max aggregation over the rows of A + I (the "Max" aggregator of Listing 1).
+
+    Returns (P, argmax): P[u,c] = max_v M[v,c] over u's row, argmax the first such v.
+    """
+    M = np.ascontiguousarray(M, np.float64)
+    w = M.shape[1]
+    P = np.zeros((g.n, w), np.float64)
+    arg = np.zeros((g.n, w), np.int32)
+    if w > 0 and g.n > 0:
+        lib().orc_aggregate_max(g.n, _p(g.row_ptr), _p(g.col_idx), _p(M), w, w, _p(P), _p(arg))
+    return P, arg
+
+
+def aggregate_max_backward(g: Graph, dP: np.ndarray, argmax: np.ndarray):
+    """Gradient of the max aggregation: dM[argmax[u,c], c] += dP[u,c]."""
+    dP = np.ascontiguousarray(dP, np.float64)
+    arg = np.ascontiguousarray(argmax, np.int32)
+    w = dP.shape[1]
+    dM = np.zeros((g.n, w), np.float64)
+    if w > 0 and g.n > 0:
+        lib().orc_aggregate_max_backward(g.n, _p(dP), w, _p(arg), _p(dM), w)
+    return dM
 
 
 def spmm(ptr, idx, val, B, want_mag: bool = False):
@@ -261,61 +299,87 @@ class SparseX:
         self.csc = dense_to_csc(X)
 
 
-def forward(g: Graph, X, Ws, bs, sparse: SparseX | None = None):
-    """Z_l = A_hat (H_l W_l) + b_l;  H_{l+1} = ReLU(Z_l) for l < L-1;  H_0 = X.
+def forward(g: Graph, X, Ws, bs, sparse: SparseX | None = None, aggs=None):
+    """Z_l = AGG_l(H_l W_l) + b_l;  H_{l+1} = ReLU(Z_l) for l < L-1;  H_0 = X.
 
-    With ``sparse`` the first transform is X_csr W_0 (Algorithm 1, Forward).
+    AGG_l is A_hat (default) or the aggregator aggs[l] ("gcn", "sum", "mean", "max");
+    a linear aggregator commutes with W, the max one is applied first:
+    Z_l = max-aggregate(H_l) W_l + b_l.  With ``sparse`` the first transform of a
+    linear layer is X_csr W_0 (Algorithm 1, Forward).
     Returns (Hs, Zs): Hs[l] is the input of layer l, Zs[l] its pre-activation.
     """
-    L = len(Ws)
-    Hs = [np.asarray(X, np.float64)]
-    Zs = []
-    for l in range(L):
-        if l == 0 and sparse is not None:
-            rp, col, val = sparse.csr
-            Mt = spmm(rp, col, val, Ws[0])
-        else:
-            Mt = matmul(Hs[l], Ws[l])
-        Z = aggregate(g, Mt, bs[l])
-        Zs.append(Z)
-        if l < L - 1:
-            Hs.append(np.maximum(Z, 0.0))
+    Hs, Zs, _ = forward_aux(g, X, Ws, bs, sparse, aggs)
     return Hs, Zs
 
 
-def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None):
+def forward_aux(g: Graph, X, Ws, bs, sparse: SparseX | None = None, aggs=None):
+    """``forward`` plus, for max layers, the saved (P, argmax) in aux[l]."""
+    L = len(Ws)
+    aggs = aggs or ["gcn"] * L
+    Hs = [np.asarray(X, np.float64)]
+    Zs, aux = [], [None] * L
+    for l in range(L):
+        if aggs[l] == "max":
+            P, arg = aggregate_max(g, Hs[l])
+            aux[l] = (P, arg)
+            Z = matmul(P, Ws[l]) + np.asarray(bs[l], np.float64)
+        else:
+            if l == 0 and sparse is not None:
+                rp, col, val = sparse.csr
+                Mt = spmm(rp, col, val, Ws[0])
+            else:
+                Mt = matmul(Hs[l], Ws[l])
+            Z = aggregate(g, Mt, bs[l], kind=aggs[l])
+        Zs.append(Z)
+        if l < L - 1:
+            Hs.append(np.maximum(Z, 0.0))
+    return Hs, Zs, aux
+
+
+def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=None, aux=None):
     """Gradients of the mean loss for every layer (Algorithm 1, Backward).
 
-    Q_l = A_hat G_l;  dW_l = H_l^T Q_l (X_csc Q_0 on the sparse path);
-    db_l = sum_i G_l[i,:];  G_{l-1} = (Q_l W_l^T) * 1[Z_{l-1} > 0].
-    Returns (dWs, dbs, Gs) with Gs[l] = dLoss/dZ_l.
+    Linear layers: Q_l = S_l^T G_l (A_hat and A + I are symmetric, the mean's transpose
+    is (A+I) D^-1);  dW_l = H_l^T Q_l (X_csc Q_0 on the sparse path);
+    G_{l-1} = (Q_l W_l^T) * 1[Z_{l-1} > 0].
+    Max layers: dW_l = P_l^T G_l;  G_{l-1} = maxgrad(G_l W_l^T) * 1[Z_{l-1} > 0].
+    db_l = sum_i G_l[i,:].  Returns (dWs, dbs, Gs) with Gs[l] = dLoss/dZ_l.
     """
     L = len(Ws)
+    aggs = aggs or ["gcn"] * L
     dWs, dbs, Gs = [None] * L, [None] * L, [None] * L
     G = np.asarray(G_last, np.float64)
     for l in range(L - 1, -1, -1):
         Gs[l] = G
-        Q = aggregate(g, G)
         dbs[l] = G.sum(axis=0)
+        Wt = np.asarray(Ws[l], np.float64).T
+        if aggs[l] == "max":
+            P, arg = aux[l]
+            dWs[l] = matmul(P.T, G)
+            if l > 0:
+                G = aggregate_max_backward(g, matmul(G, Wt), arg) * (Zs[l - 1] > 0.0)
+            continue
+        Q = aggregate(g, G, kind=TRANSPOSE[aggs[l]])
         if l == 0 and sparse is not None:
             cp, row, val = sparse.csc
             dWs[l] = spmm(cp, row, val, Q)
         else:
             dWs[l] = matmul(Hs[l].T, Q)
         if l > 0:
-            G = matmul(Q, np.asarray(Ws[l], np.float64).T) * (Zs[l - 1] > 0.0)
+            G = matmul(Q, Wt) * (Zs[l - 1] > 0.0)
     return dWs, dbs, Gs
 
 
 def epoch(g: Graph, X, y, Ws, bs, mW, vW, mb, vb, t: int, sparse: SparseX | None = None,
-          lr=0.01, b1=0.9, b2=0.999, eps=1e-8):
+          lr=0.01, b1=0.9, b2=0.999, eps=1e-8, aggs=None):
     """One training epoch: forward, softmax-CE loss, backward, Adam step t (t >= 1).
 
+    aggs: per-layer aggregator ("gcn" default, "sum", "mean", "max").
     Returns a dict with loss, activations, gradients and updated parameters/state.
     """
-    Hs, Zs = forward(g, X, Ws, bs, sparse)
+    Hs, Zs, aux = forward_aux(g, X, Ws, bs, sparse, aggs)
     loss, G, _ = softmax_ce(Zs[-1], y)
-    dWs, dbs, Gs = backward(g, Hs, Zs, G, Ws, sparse)
+    dWs, dbs, Gs = backward(g, Hs, Zs, G, Ws, sparse, aggs, aux)
     nW, nmW, nvW, nb, nmb, nvb = [], [], [], [], [], []
     for l in range(len(Ws)):
         a, m_, v_ = adam(Ws[l], dWs[l], mW[l], vW[l], t, lr, b1, b2, eps)
@@ -323,14 +387,15 @@ def epoch(g: Graph, X, y, Ws, bs, mW, vW, mb, vb, t: int, sparse: SparseX | None
         a, m_, v_ = adam(bs[l], dbs[l], mb[l], vb[l], t, lr, b1, b2, eps)
         nb.append(a), nmb.append(m_), nvb.append(v_)
     return dict(loss=loss, Hs=Hs, Zs=Zs, G=G, Gs=Gs, dWs=dWs, dbs=dbs, Ws=nW, bs=nb, mW=nmW,
-                vW=nvW, mb=nmb, vb=nvb)
+                vW=nvW, mb=nmb, vb=nvb, aux=aux)
 
 
-def dense_operator(g: Graph) -> np.ndarray:
-    """A_hat as a dense fp64 matrix from the CSR (small graphs only)."""
+def dense_operator(g: Graph, kind: str = "gcn") -> np.ndarray:
+    """The aggregation operator (A_hat by default) as a dense fp64 matrix (small graphs only)."""
     A = np.zeros((g.n, g.n), np.float64)
     for u in range(g.n):
         for e in range(g.row_ptr[u], g.row_ptr[u + 1]):
             v = g.col_idx[e]
-            A[u, v] = 1.0 / np.sqrt(float(g.deg[u]) * float(g.deg[v]))
+            du, dv = float(g.deg[u]), float(g.deg[v])
+            A[u, v] = {"gcn": 1.0 / np.sqrt(du * dv), "sum": 1.0, "mean": 1.0 / du, "mean_t": 1.0 / dv}[kind]
     return A

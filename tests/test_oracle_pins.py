@@ -475,3 +475,167 @@ def test_epochs_match_torch_training(orc):
     for l in range(2):
         np.testing.assert_allclose(st["Ws"][l], Wt[l].detach().numpy(), atol=1e-12)
         np.testing.assert_allclose(st["bs"][l], bt[l].detach().numpy(), atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# other aggregators: sum (A + I), mean (D^-1 (A + I)) and its transpose, max
+# ---------------------------------------------------------------------------
+
+
+def brute_operator(n, src, dst, kind):
+    """Dense aggregation operator from an adjacency matrix built entry by entry."""
+    A = np.zeros((n, n))
+    for u, v in zip(src, dst):
+        if u != v:
+            A[u, v] = 1.0
+            A[v, u] = 1.0
+    A += np.eye(n)
+    d = A.sum(axis=1)
+    return {"sum": A, "mean": A / d[:, None], "mean_t": A / d[None, :]}[kind]
+
+
+@pytest.mark.parametrize("kind", ["sum", "mean", "mean_t"])
+@pytest.mark.parametrize("seed", range(3))
+def test_linear_aggregators_match_dense_brute_force(orc, kind, seed):
+    rng = np.random.default_rng(100 + seed)
+    n = 40
+    src, dst = random_edges(rng, n, 90)
+    g = orc.build_csr(n, src, dst)
+    M = rng.standard_normal((n, 5))
+    b = rng.standard_normal(5)
+    S = brute_operator(n, src.tolist(), dst.tolist(), kind)
+    Z, mag = orc.aggregate(g, M, b, want_mag=True, kind=kind)
+    np.testing.assert_allclose(Z, S @ M + b, atol=1e-12)
+    np.testing.assert_allclose(mag, np.abs(S) @ np.abs(M) + np.abs(b), atol=1e-12)
+    np.testing.assert_allclose(orc.dense_operator(g, kind), S, atol=1e-15)
+
+
+def test_linear_aggregator_closed_forms(orc):
+    n = 9
+    s, d = star(n - 1)
+    g = orc.build_csr(n, s, d)
+    ones = np.ones((n, 1))
+    # sum of ones is the degree: hub n, leaves 2
+    np.testing.assert_array_equal(orc.aggregate(g, ones, kind="sum")[:, 0], [n] + [2] * (n - 1))
+    # the mean keeps constant columns; the transpose of the mean sums 1/d over a row
+    np.testing.assert_allclose(orc.aggregate(g, 3.5 * ones, kind="mean"), 3.5 * ones, rtol=1e-15)
+    np.testing.assert_allclose(orc.aggregate(g, ones, kind="mean_t")[0, 0], 1 / n + (n - 1) / 2, rtol=1e-15)
+    # complete graph: the mean is the column mean
+    s, d = complete(6)
+    g = orc.build_csr(6, s, d)
+    M = np.arange(18.0).reshape(6, 3)
+    np.testing.assert_allclose(orc.aggregate(g, M, kind="mean"), np.tile(M.mean(0), (6, 1)), rtol=1e-15)
+
+
+def brute_max(n, rows, M):
+    P = np.zeros_like(M)
+    arg = np.zeros(M.shape, np.int32)
+    for u in range(n):
+        for c in range(M.shape[1]):
+            vals = [M[v, c] for v in rows[u]]
+            best = max(vals)
+            P[u, c] = best
+            arg[u, c] = rows[u][vals.index(best)]  # first maximal, columns ascending
+    return P, arg
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_max_aggregation_brute_force_with_ties(orc, seed):
+    rng = np.random.default_rng(200 + seed)
+    n = 35
+    src, dst = random_edges(rng, n, 80)
+    g = orc.build_csr(n, src, dst)
+    rows = brute_rows(n, src.tolist(), dst.tolist())
+    M = rng.integers(-2, 3, (n, 6)).astype(np.float64)  # small integers: many ties
+    P, arg = orc.aggregate_max(g, M)
+    Pb, argb = brute_max(n, rows, M)
+    np.testing.assert_array_equal(P, Pb)
+    np.testing.assert_array_equal(arg, argb)
+    assert (P >= M).all()  # the row includes the node itself
+    # gradient: each output passes its gradient to the one input it copied
+    dP = rng.standard_normal((n, 6))
+    dM = orc.aggregate_max_backward(g, dP, arg)
+    want = np.zeros_like(dM)
+    for u in range(n):
+        for v in rows[u]:  # gather form over the symmetric rows
+            want[u] += dP[v] * (arg[v] == u)
+    np.testing.assert_allclose(dM, want, atol=1e-14)
+    np.testing.assert_allclose(dM.sum(0), dP.sum(0), atol=1e-12)
+
+
+def torch_model_aggs(n, src, dst, X, Ws, bs, y, aggs):
+    """Reference model in torch autograd: dense operators for the linear aggregators, a
+    padded neighbour gather with max over the neighbourhood for the max one."""
+    rows = brute_rows(n, src, dst)
+    dmax = max(len(r) for r in rows)
+    nb = torch.tensor([r + [r[0]] * (dmax - len(r)) for r in rows])  # pad with a repeat
+    H = torch.tensor(np.asarray(X, np.float64))
+    Wt = [torch.tensor(np.asarray(w, np.float64), requires_grad=True) for w in Ws]
+    bt = [torch.tensor(np.asarray(b, np.float64), requires_grad=True) for b in bs]
+    Zs = []
+    for l, a in enumerate(aggs):
+        if a == "max":
+            P = H[nb].max(dim=1).values  # (n, dmax, w) -> (n, w)
+            Z = P @ Wt[l] + bt[l]
+        else:
+            S = torch.tensor(brute_ahat(n, src, dst) if a == "gcn" else brute_operator(n, src, dst, a))
+            Z = S @ (H @ Wt[l]) + bt[l]
+        Zs.append(Z)
+        H = torch.relu(Z) if l < len(Ws) - 1 else Z
+    loss = torch.nn.functional.cross_entropy(Zs[-1], torch.tensor(y, dtype=torch.long))
+    loss.backward()
+    return loss.item(), [z.detach().numpy() for z in Zs], [w.grad.numpy() for w in Wt], \
+        [b.grad.numpy() for b in bt]
+
+
+@pytest.mark.parametrize("aggs", [("max", "sum", "mean"), ("sum", "max", "gcn"), ("mean", "mean", "max")])
+def test_aggregator_models_match_torch_autograd(orc, aggs):
+    src, dst, X, Ws, bs, y = tiny_problem(7, n=30, widths=(6, 5, 4, 3))
+    n = X.shape[0]
+    g = orc.build_csr(n, src, dst)
+    Hs, Zs, aux = orc.forward_aux(g, X, Ws, bs, aggs=list(aggs))
+    loss, G, _ = orc.softmax_ce(Zs[-1], y)
+    dWs, dbs, _ = orc.backward(g, Hs, Zs, G, Ws, aggs=list(aggs), aux=aux)
+    tl, tZ, tdW, tdb = torch_model_aggs(n, src.tolist(), dst.tolist(), X, Ws, bs, y, aggs)
+    assert loss == pytest.approx(tl, rel=1e-12)
+    for l in range(len(Ws)):
+        np.testing.assert_allclose(Zs[l], tZ[l], atol=1e-12)
+        np.testing.assert_allclose(dWs[l], tdW[l], atol=1e-12)
+        np.testing.assert_allclose(dbs[l], tdb[l], atol=1e-13)
+
+
+def test_max_model_central_differences(orc):
+    """Max-aggregator model against central differences (inputs away from kinks and ties)."""
+    for seed in range(200):
+        src, dst, X, Ws, bs, y = tiny_problem(3000 + seed, n=12, widths=(4, 5, 3))
+        g = orc.build_csr(12, src, dst)
+        aggs = ["max", "max"]
+        Hs, Zs, aux = orc.forward_aux(g, X, Ws, bs, aggs=aggs)
+        # distinct values near every max: second-best at least 1e-3 below the best
+        ok = np.abs(Zs[0]).min() > 1e-3
+        for l in range(2):
+            M = Hs[l]
+            for u in range(12):
+                row = g.col_idx[g.row_ptr[u]:g.row_ptr[u + 1]]
+                srt = np.sort(M[row], axis=0)
+                if row.size > 1 and (srt[-1] - srt[-2]).min() < 1e-3:
+                    ok = False
+        if ok:
+            break
+    else:
+        pytest.fail("no kink-free sample")
+    loss, G, _ = orc.softmax_ce(Zs[-1], y)
+    dWs, dbs, _ = orc.backward(g, Hs, Zs, G, Ws, aggs=aggs, aux=aux)
+
+    def f(Ws_, bs_):
+        _, Z_ = orc.forward(g, X, Ws_, bs_, aggs=aggs)
+        return orc.softmax_ce(Z_[-1], y)[0]
+
+    h = 1e-6
+    for l in range(2):
+        for idx in np.ndindex(Ws[l].shape):
+            Wp = [w.copy() for w in Ws]
+            Wm = [w.copy() for w in Ws]
+            Wp[l][idx] += h
+            Wm[l][idx] -= h
+            assert (f(Wp, bs) - f(Wm, bs)) / (2 * h) == pytest.approx(dWs[l][idx], abs=1e-8)
