@@ -135,13 +135,30 @@ typedef struct gcn_feature_info {
 } gcn_feature_info;
 
 /* One GCN layer l: Z = A_hat (H W) + b, H_out = act(Z). */
+/*
+ * Neighbourhood aggregators (Section III-A: GCN's normalised mean, GIN's sum,
+ * mean and max; Listing 1 trains with "Max").  All aggregate over the CSR row of
+ * A + I, the node itself included:
+ *   GCN_AGG_NORM    A_hat = D^-1/2 (A + I) D^-1/2  (the default)
+ *   GCN_AGG_SUM     A + I                           (GIN with epsilon = 0)
+ *   GCN_AGG_MEAN    D^-1 (A + I)
+ *   GCN_AGG_MEAN_T  (A + I) D^-1, the transpose of the mean (its gradient;
+ *                   gcn_aggregate only)
+ *   GCN_AGG_MAX     elementwise max over the row, with the first (lowest-column)
+ *                   maximiser saved for the gradient
+ * A linear aggregator commutes with W, so its layer may run either order; a max
+ * layer is always aggregate-first: Z = max-aggregate(H_in) W + b.
+ */
+enum { GCN_AGG_NORM = 0, GCN_AGG_SUM = 1, GCN_AGG_MEAN = 2, GCN_AGG_MEAN_T = 3, GCN_AGG_MAX = 4 };
+
 typedef struct gcn_layer {
   int32_t f_in, f_out;  /* widths of H_in and H_out */
-  int64_t ld_in;        /* pitch of H_in and of the saved A_hat H_in (aggregate-first) */
+  int64_t ld_in;        /* pitch of H_in and of the saved aggregate of H_in (aggregate-first) */
   int64_t ld_out;       /* pitch of H_out / Z and of G = dLoss/dZ */
   int32_t act;          /* GCN_ACT_RELU (hidden), GCN_ACT_NONE, GCN_ACT_SOFTMAX_CE (last) */
   int32_t order;        /* GCN_ORDER_AUTO or a forced evaluation order */
   int32_t index;        /* layer number l (0 = input layer) */
+  int32_t agg;          /* GCN_AGG_NORM (0), GCN_AGG_SUM, GCN_AGG_MEAN or GCN_AGG_MAX */
 } gcn_layer;
 
 /*
@@ -183,8 +200,9 @@ gcn_status gcn_feature_stats(const float* d_X, int32_t n, int32_t f, int64_t ldx
                              void* d_ws, size_t* ws_bytes, hipStream_t stream);
 
 /* Evaluation order the library uses for a layer: GCN_TRANSFORM_FIRST
- * (A_hat (H W)) or GCN_AGGREGATE_FIRST ((A_hat H) W).  Both are the same
- * product; the cheaper one aggregates fewer columns per epoch.  x_sparse: the
+ * (S (H W)) or GCN_AGGREGATE_FIRST ((S H) W) for the layer's aggregator S.  For
+ * a linear aggregator both are the same product and the cheaper one aggregates
+ * fewer columns per epoch; a max layer is always aggregate-first.  x_sparse: the
  * layer's input is sparse X. */
 int32_t gcn_layer_order(const gcn_layer* L, int32_t x_sparse);
 
@@ -200,9 +218,12 @@ int32_t gcn_layer_order(const gcn_layer* L, int32_t x_sparse);
  *   (device fp32 scalar) = (1/n) sum_i (logsumexp(Z_i) - Z_i,labels_i);
  *   d_labels: n int32 in [0, f_out).  The logits themselves are written to
  *   d_logits (pitch ld_out) when it is non-NULL.
- * d_saved: n x f_in (pitch ld_in), receives A_hat H_in when the layer is
- * evaluated aggregate-first (needed again by gcn_layer_bwd); may be NULL
- * otherwise.
+ * The aggregator is L->agg (A_hat for GCN_AGG_NORM).
+ * d_saved: n x f_in (pitch ld_in), receives the aggregate S H_in when the layer
+ * is evaluated aggregate-first (needed again by gcn_layer_bwd); may be NULL
+ * otherwise.  A max layer needs twice that: the maxima (n x ld_in fp32), then the
+ * maximisers (n x ld_in int32 node ids) at d_saved + n * ld_in.  A max layer takes
+ * dense input only (GCN_E_UNSUPPORTED for sparse X) and f_in <= 256.
  */
 gcn_status gcn_layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* d_Hin,
                          const gcn_sparse_x* x, const float* d_W, const float* d_b,
@@ -214,12 +235,13 @@ gcn_status gcn_layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* d_
  * Asynchronous.
  *
  * d_G = dLoss/dZ (n x f_out, pitch ld_out).  Writes d_dW = dLoss/dW (f_in x
- * f_out, pitch f_out) and d_db = sum_i G[i,:] (f_out).  With Q = A_hat G
- * (A_hat is symmetric): dW = H_in^T Q, or X^T Q via X_csc on the sparse path.
- * When d_Gprev != NULL (layers above the first) it receives the gradient of the
- * previous layer's pre-activation: (Q W^T) * 1[H_in > 0] (n x f_in, pitch
- * ld_in).  d_saved is the buffer gcn_layer_fwd filled for aggregate-first
- * layers.
+ * f_out, pitch f_out) and d_db = sum_i G[i,:] (f_out).  With Q = S^T G (A_hat
+ * and A + I are symmetric; the mean's transpose is (A + I) D^-1): dW = H_in^T Q,
+ * or X^T Q via X_csc on the sparse path.  When d_Gprev != NULL (layers above the
+ * first) it receives the gradient of the previous layer's pre-activation:
+ * (Q W^T) * 1[H_in > 0] (n x f_in, pitch ld_in).  Max layers: dW = P^T G with the
+ * saved maxima P, and G_prev routes (G W^T)[u,c] to the saved maximiser of (u, c).
+ * d_saved is the buffer gcn_layer_fwd filled for aggregate-first layers.
  */
 gcn_status gcn_layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* d_G,
                          const float* d_Hin, const gcn_sparse_x* x, const float* d_saved,
@@ -229,8 +251,8 @@ gcn_status gcn_layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* d_
 /*
  * Whole model for gcn_epoch.  Host arrays of n_layers device pointers each.
  * act[l] (l < n_layers - 1) holds H_{l+1}; grad[l] holds G_l = dLoss/dZ_l;
- * saved[l] holds A_hat H_l for aggregate-first layers (NULL entries allowed
- * otherwise).  Adam state m*, v* starts at zero; step counts completed steps.
+ * saved[l] holds the aggregate of H_l for aggregate-first layers (twice that
+ * size for max layers, see gcn_layer_fwd; NULL entries allowed otherwise).  Adam state m*, v* starts at zero; step counts completed steps.
  */
 typedef struct gcn_model {
   int32_t n_layers;
@@ -272,16 +294,41 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
  * ---------------------------------------------------------------------- */
 
 /*
- * gcn_aggregate -- Z = A_hat M (+ b) over all n rows (Section III-A;
- * Algorithm 3's row-parallel, atomic-free aggregation).  Asynchronous.
+ * gcn_aggregate -- Z = S M (+ b) over all n rows, S = A_hat (GCN_AGG_NORM), A + I
+ * (GCN_AGG_SUM), D^-1 (A + I) (GCN_AGG_MEAN) or (A + I) D^-1 (GCN_AGG_MEAN_T)
+ * (Section III-A; Algorithm 3's row-parallel, atomic-free aggregation).  Asynchronous.
  * d_M: n x w (pitch ldm).  d_bias: w or NULL.  epi: GCN_EPI_NONE, GCN_EPI_RELU
  * (max(Z, 0)) or GCN_EPI_MASK (Z * 1[mask > 0], d_mask n x w, pitch ldmask).
  * d_Z: n x w (pitch ldz); must not overlap d_M.  The workspace holds the chunk
  * sums of split hub rows (g->split.n_chunk x w floats, rounded up).
  */
-gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm,
+gcn_status gcn_aggregate(const gcn_graph* g, int32_t agg, int32_t w, const float* d_M, int64_t ldm,
                          const float* d_bias, int32_t epi, const float* d_mask, int64_t ldmask,
                          float* d_Z, int64_t ldz, void* d_ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
+ * gcn_aggregate_max -- max aggregation (GCN_AGG_MAX): P[u,c] = max over the row
+ * of A + I of M[v,c] and arg[u,c] = the first v (lowest column) attaining it.
+ * Asynchronous.  d_M: n x w (pitch ldm); d_P: n x w fp32 (pitch ldp); d_arg:
+ * n x w int32 (pitch ldarg).  w <= 256 (64 when a pitch is not a multiple of 4 or
+ * a buffer is not 16-byte aligned): else GCN_E_UNSUPPORTED.  No workspace (the
+ * size query returns 0).
+ */
+gcn_status gcn_aggregate_max(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm, float* d_P,
+                             int64_t ldp, int32_t* d_arg, int64_t ldarg, void* d_ws, size_t* ws_bytes,
+                             hipStream_t stream);
+
+/*
+ * gcn_aggregate_max_bwd -- gradient of the max aggregation: dM[u,c] = sum over
+ * v in the row of u of dP[v,c] * [arg[v,c] == u] (A + I is symmetric, so this
+ * gathers every output that u supplied), times 1[mask[u,c] > 0] when d_mask is
+ * non-NULL.  Asynchronous; fixed summation order, no atomics.  d_dP, d_arg as
+ * produced with gcn_aggregate_max (n x w); d_dM: n x w (pitch ldo), must not
+ * overlap the inputs.  Same width limits; no workspace.
+ */
+gcn_status gcn_aggregate_max_bwd(const gcn_graph* g, int32_t w, const float* d_dP, int64_t ldd,
+                                 const int32_t* d_arg, int64_t ldarg, const float* d_mask, int64_t ldmask,
+                                 float* d_dM, int64_t ldo, void* d_ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
  * gcn_gemm -- dense fp32 product on the matrix cores (the dense-path GEMM of

@@ -94,12 +94,24 @@ struct First {
   float w;
 };
 
+// Weight of entry e (column j) by the aggregation kind (wave-uniform branch).
+__device__ __forceinline__ float entry_weight(const AggParams& p, int64_t e, int j) {
+  if (p.kind == AGG_W_VAL) return p.val[e];
+  if (p.kind == AGG_W_COLMEAN) return 1.f / (float)p.deg[j];
+  return 1.f;
+}
+
+// Factor applied to a row's sum: 1 / deg[row] for the mean, else 1.
+__device__ __forceinline__ float row_scale(const AggParams& p, int64_t row) {
+  return p.kind == AGG_W_ROWMEAN ? 1.f / (float)p.deg[row] : 1.f;
+}
+
 template <int LANES>
 __device__ __forceinline__ First load_first(const AggParams& p, int64_t beg, int64_t end, const Lanes& L) {
   First f{0, 0.f};
   if (beg + L.lig < end) {
     f.j = p.col[beg + L.lig];
-    f.w = p.val[beg + L.lig];
+    f.w = entry_weight(p, beg + L.lig, f.j);
   }
   return f;
 }
@@ -120,7 +132,7 @@ __device__ __forceinline__ typename Vec<VEC>::T accumulate(const AggParams& p, i
     float my_w = first.w;
     if (base != beg) {
       my_j = L.lig < cnt ? p.col[base + L.lig] : 0;
-      my_w = L.lig < cnt ? p.val[base + L.lig] : 0.f;
+      my_w = L.lig < cnt ? entry_weight(p, base + L.lig, my_j) : 0.f;
     }
     for (int t = 0; t < cnt; t += slots * UNR) {
       int jj[UNR];

@@ -41,11 +41,12 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
                                            const Lanes& L, bool cok) {
   using V = Vec<VEC>;
   const int c0 = L.c0;
+  const float sc = row_scale(p, row);
   float z[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) {
     const int c = c0 + i;
-    z[i] = V::get(acc, i);
+    z[i] = sc * V::get(acc, i);
     if (p.bias && c < p.w) z[i] += p.bias[c];
   }
   if constexpr (EPI == AGG_SOFTMAX) {
@@ -275,6 +276,20 @@ gcn_status launch_aggregate_long_rows(const AggParams& p, const gcn_split* split
 }
 
 int agg_slots(int lanes, int64_t nnz, int64_t rows) { return pick_slots(lanes, nnz, rows); }
+
+namespace {
+__global__ void k_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i <= n) row_ptr[i] = i;
+  if (i < n) col[i] = (int32_t)i;
+}
+}  // namespace
+
+gcn_status launch_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col, hipStream_t s) {
+  hipLaunchKernelGGL(k_identity_csr, dim3((unsigned)ceil_div((int64_t)n + 1, 256)), dim3(256), 0, s, n, row_ptr,
+                     col);
+  return check_launch("identity operator");
+}
 
 size_t aggregate_workspace(const gcn_split* split, int32_t w) {
   if (!has_split(split)) return 0;

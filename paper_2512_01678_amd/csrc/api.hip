@@ -62,6 +62,12 @@ gcn_status check_layer(const gcn_layer* L, const char* who) {
     return fail(GCN_E_INVALID, std::string(who) + ": unknown order");
   if (L->act == GCN_ACT_SOFTMAX_CE && L->f_out > 256)
     return fail(GCN_E_UNSUPPORTED, std::string(who) + ": softmax cross-entropy needs f_out <= 256");
+  if (L->agg != GCN_AGG_NORM && L->agg != GCN_AGG_SUM && L->agg != GCN_AGG_MEAN && L->agg != GCN_AGG_MAX)
+    return fail(GCN_E_INVALID, std::string(who) + ": unknown aggregator");
+  if (L->agg == GCN_AGG_MAX && L->order == GCN_TRANSFORM_FIRST)
+    return fail(GCN_E_INVALID, std::string(who) + ": a max layer aggregates first");
+  if (L->agg == GCN_AGG_MAX && L->f_in > 256)
+    return fail(GCN_E_UNSUPPORTED, std::string(who) + ": max aggregation needs f_in <= 256");
   return GCN_OK;
 }
 
@@ -78,6 +84,7 @@ gcn_status check_sparse(const gcn_sparse_x* x, const gcn_graph* g, const gcn_lay
 int64_t pitch4(int64_t w) { return round_up(w, 4); }
 
 int32_t resolve_order(const gcn_layer* L, bool x_sparse) {
+  if (L->agg == GCN_AGG_MAX) return GCN_AGGREGATE_FIRST;  // max does not commute with W
   if (L->order != GCN_ORDER_AUTO) return L->order;
   if (L->act == GCN_ACT_SOFTMAX_CE || x_sparse) return GCN_TRANSFORM_FIRST;
   // aggregate-first aggregates f_in columns forward (and again backward above
@@ -94,8 +101,21 @@ bool af_fusable(int32_t f_in) {
   return gemm_bf16x6_mode() && f_in > 32 && f_in <= 128;
 }
 
-AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, float* Z, int64_t ldz) {
+// The aggregator that carries gradients back: A_hat and A + I are symmetric; the
+// mean's transpose is (A + I) D^-1.
+int32_t agg_transpose(int32_t agg) {
+  if (agg == GCN_AGG_MEAN) return GCN_AGG_MEAN_T;
+  if (agg == GCN_AGG_MEAN_T) return GCN_AGG_MEAN;
+  return agg;
+}
+
+AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, float* Z, int64_t ldz,
+                    int32_t agg = GCN_AGG_NORM) {
   AggParams p{};
+  p.deg = g->deg;
+  p.kind = agg == GCN_AGG_SUM ? AGG_W_ONE
+           : agg == GCN_AGG_MEAN ? AGG_W_ROWMEAN
+           : agg == GCN_AGG_MEAN_T ? AGG_W_COLMEAN : AGG_W_VAL;
   p.n = g->n;
   p.row_ptr = g->row_ptr;
   p.col = g->col_idx;
@@ -138,15 +158,66 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
   if (order == GCN_AGGREGATE_FIRST) {
-    // P = A_hat H_in (kept for the backward pass), then H_out = act(P W + b): one fused
-    // kernel when the widths allow it (bf16x6 mode), else an aggregation and a GEMM.
-    // The workspace covers both, so a size query made without buffers stays valid.
-    const bool fusable = af_fusable(L->f_in);
+    // P = S H_in (kept for the backward pass), then H_out = act(P W + b): one fused
+    // kernel when the widths allow it (bf16x6 mode, linear S), else an aggregation and a
+    // GEMM.  The workspace covers both, so a size query made without buffers stays valid.
+    // With the softmax cross-entropy, Z = P W + b goes through the loss epilogue of an
+    // aggregation over the identity operator.
+    const bool softmax = L->act == GCN_ACT_SOFTMAX_CE;
+    const bool fusable = af_fusable(L->f_in) && L->agg != GCN_AGG_MAX && !softmax;
     size_t need = aggregate_workspace(&g->split, L->f_in);
     if (fusable) need = std::max(need, agg_gemm_workspace(&g->split, L->f_in, L->f_out));
     void* aws = a.take<char>((int64_t)need);
-    if (run) {
+    const int64_t ldz = pitch4(L->f_out);
+    float* Zs = softmax ? a.take<float>((int64_t)n * ldz) : nullptr;
+    int64_t* id_ptr = softmax ? a.take<int64_t>((int64_t)n + 1) : nullptr;
+    int32_t* id_col = softmax ? a.take<int32_t>(n) : nullptr;
+    float* row_loss = softmax ? a.take<float>(n) : nullptr;
+    void* cws = softmax ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+    if (run && L->agg == GCN_AGG_MAX) {
       AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in);
+      int32_t* arg = reinterpret_cast<int32_t*>(saved + (int64_t)n * L->ld_in);
+      GCN_TRY(launch_aggregate_max(p, g->nnz, saved, L->ld_in, arg, L->ld_in, s));
+    }
+    if (run && softmax) {
+      if (L->agg != GCN_AGG_MAX) {
+        AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in, L->agg);
+        GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
+      }
+      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Zs, ldz);
+      q.bias = b;
+      GCN_TRY(launch_gemm(q, nullptr, s));
+      GCN_TRY(launch_identity_csr(n, id_ptr, id_col, s));
+      AggParams z{};
+      z.n = n;
+      z.row_ptr = id_ptr;
+      z.col = id_col;
+      z.kind = AGG_W_ONE;
+      z.M = Zs;
+      z.ldm = ldz;
+      z.w = L->f_out;
+      z.Z = Hout;
+      z.ldz = L->ld_out;
+      z.epi = AGG_SOFTMAX;
+      z.labels = labels;
+      z.row_loss = row_loss;
+      z.logits = logits;
+      z.ldl = L->ld_out;
+      z.inv_n = n > 0 ? 1.f / (float)n : 0.f;
+      z.tag = "softmax_ce";
+      GCN_TRY(launch_aggregate(z, n, nullptr, nullptr, s));
+      GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
+      return GCN_OK;
+    }
+    if (run && L->agg == GCN_AGG_MAX) {
+      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
+      q.bias = b;
+      q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
+      GCN_TRY(launch_gemm(q, nullptr, s));
+      return GCN_OK;
+    }
+    if (run) {
+      AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in, L->agg);
       if (fusable && agg_gemm_supported(L->f_in, L->ld_in, L->ld_in, Hin, saved)) {
         GCN_TRY(launch_agg_gemm(p, g->nnz, &g->split, W, L->f_out, L->f_out, b, L->act == GCN_ACT_RELU, Hout,
                                 L->ld_out, aws, s));
@@ -185,7 +256,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
     GCN_TRY(launch_gemm(q, nullptr, s));
   }
-  AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out);
+  AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out, L->agg);
   p.bias = b;
   if (L->act == GCN_ACT_RELU) p.epi = AGG_RELU;
   if (L->act == GCN_ACT_SOFTMAX_CE) {
@@ -222,7 +293,13 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     if (Gprev) {
       GemmParams t = gemm(n, L->f_in, L->f_out, G, L->ld_out, false, W, L->f_out, true, T, ldt);
       GCN_TRY(launch_gemm(t, nullptr, s));
-      AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in);
+      AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in, agg_transpose(L->agg));
+      if (L->agg == GCN_AGG_MAX) {
+        // each (G W^T)[v,c] goes back to the saved maximiser of (v, c)
+        const int32_t* arg = reinterpret_cast<const int32_t*>(saved + (int64_t)n * L->ld_in);
+        GCN_TRY(launch_aggregate_max_bwd(p, g->nnz, arg, L->ld_in, Hin, L->ld_in, Gprev, L->ld_in, s));
+        return GCN_OK;
+      }
       p.epi = AGG_MASK;
       p.mask = Hin;
       p.ldmask = L->ld_in;
@@ -230,7 +307,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     }
     return GCN_OK;
   }
-  // transform-first: Q = A_hat G; dW = H_in^T Q (X_csc Q); G_prev = (Q W^T) * 1[H_in > 0]
+  // transform-first: Q = S^T G; dW = H_in^T Q (X_csc Q); G_prev = (Q W^T) * 1[H_in > 0]
   const int64_t ldq = pitch4(L->f_out);
   float* Q = a.take<float>((int64_t)n * ldq);
   GemmParams dw = gemm(L->f_in, L->f_out, n, Hin, L->ld_in, true, Q, ldq, false, dW, L->f_out);
@@ -239,7 +316,8 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
                                    x ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
   void* aws = a.take<char>((int64_t)agg_need);
   if (!run) return GCN_OK;
-  GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq), g->nnz, &g->split, aws, s));
+  GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq, agg_transpose(L->agg)), g->nnz,
+                           &g->split, aws, s));
   if (x) {
     AggParams p{};
     p.n = x->f;
@@ -280,8 +358,6 @@ gcn_status validate_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin
   const int32_t order = resolve_order(L, x != nullptr);
   if (order == GCN_AGGREGATE_FIRST) {
     if (x) return fail(GCN_E_UNSUPPORTED, std::string(who) + ": aggregate-first needs dense input");
-    if (L->act == GCN_ACT_SOFTMAX_CE)
-      return fail(GCN_E_UNSUPPORTED, std::string(who) + ": aggregate-first with softmax cross-entropy");
     if (!saved) return fail(GCN_E_INVALID, std::string(who) + ": aggregate-first needs d_saved");
   }
   if (L->act == GCN_ACT_SOFTMAX_CE && (!labels || !loss))
@@ -331,7 +407,7 @@ const char* gcn_status_string(gcn_status s) {
 
 const char* gcn_last_error(void) { return g_err.c_str(); }
 
-int32_t gcn_version(void) { return 2; }
+int32_t gcn_version(void) { return 3; }
 
 int32_t gcn_layer_order(const gcn_layer* L, int32_t x_sparse) {
   return L ? resolve_order(L, x_sparse != 0) : GCN_TRANSFORM_FIRST;
@@ -478,11 +554,13 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
   return GCN_OK;
 }
 
-gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm, const float* d_bias,
-                         int32_t epi, const float* d_mask, int64_t ldmask, float* d_Z, int64_t ldz, void* d_ws,
-                         size_t* ws_bytes, hipStream_t stream) {
+gcn_status gcn_aggregate(const gcn_graph* g, int32_t agg, int32_t w, const float* d_M, int64_t ldm,
+                         const float* d_bias, int32_t epi, const float* d_mask, int64_t ldmask, float* d_Z,
+                         int64_t ldz, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
   g_err.clear();
   GCN_TRY(check_graph(g, "gcn_aggregate"));
+  if (agg < GCN_AGG_NORM || agg > GCN_AGG_MEAN_T)
+    return fail(GCN_E_INVALID, "gcn_aggregate: aggregator must be NORM, SUM, MEAN or MEAN_T");
   if (w < 0 || ldm < w || ldz < w) return fail(GCN_E_INVALID, "gcn_aggregate: bad width or pitch");
   if (epi < GCN_EPI_NONE || epi > GCN_EPI_MASK) return fail(GCN_E_INVALID, "gcn_aggregate: unknown epilogue");
   if (epi == GCN_EPI_MASK && (!d_mask || ldmask < w)) return fail(GCN_E_INVALID, "gcn_aggregate: mask missing");
@@ -490,12 +568,43 @@ gcn_status gcn_aggregate(const gcn_graph* g, int32_t w, const float* d_M, int64_
   GCN_TRY(ws_protocol(d_ws, ws_bytes, aggregate_workspace(&g->split, w), "gcn_aggregate", &query));
   if (query) return GCN_OK;
   if (g->n > 0 && w > 0 && (!d_M || !d_Z)) return fail(GCN_E_INVALID, "gcn_aggregate: d_M and d_Z are required");
-  AggParams p = graph_agg(g, w, d_M, ldm, d_Z, ldz);
+  AggParams p = graph_agg(g, w, d_M, ldm, d_Z, ldz, agg);
   p.bias = d_bias;
   p.epi = epi == GCN_EPI_RELU ? AGG_RELU : (epi == GCN_EPI_MASK ? AGG_MASK : AGG_NONE);
   p.mask = d_mask;
   p.ldmask = ldmask;
   return launch_aggregate(p, g->nnz, &g->split, d_ws, stream);
+}
+
+gcn_status gcn_aggregate_max(const gcn_graph* g, int32_t w, const float* d_M, int64_t ldm, float* d_P,
+                             int64_t ldp, int32_t* d_arg, int64_t ldarg, void* d_ws, size_t* ws_bytes,
+                             hipStream_t stream) {
+  g_err.clear();
+  GCN_TRY(check_graph(g, "gcn_aggregate_max"));
+  if (w < 0 || ldm < w || ldp < w || ldarg < w) return fail(GCN_E_INVALID, "gcn_aggregate_max: bad width or pitch");
+  if (w > 256) return fail(GCN_E_UNSUPPORTED, "gcn_aggregate_max: width above 256");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, 0, "gcn_aggregate_max", &query));
+  if (query) return GCN_OK;
+  if (g->n > 0 && w > 0 && (!d_M || !d_P || !d_arg)) return fail(GCN_E_INVALID, "gcn_aggregate_max: NULL buffer");
+  return launch_aggregate_max(graph_agg(g, w, d_M, ldm, d_P, ldp), g->nnz, d_P, ldp, d_arg, ldarg, stream);
+}
+
+gcn_status gcn_aggregate_max_bwd(const gcn_graph* g, int32_t w, const float* d_dP, int64_t ldd,
+                                 const int32_t* d_arg, int64_t ldarg, const float* d_mask, int64_t ldmask,
+                                 float* d_dM, int64_t ldo, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  GCN_TRY(check_graph(g, "gcn_aggregate_max_bwd"));
+  if (w < 0 || ldd < w || ldarg < w || ldo < w || (d_mask && ldmask < w))
+    return fail(GCN_E_INVALID, "gcn_aggregate_max_bwd: bad width or pitch");
+  if (w > 256) return fail(GCN_E_UNSUPPORTED, "gcn_aggregate_max_bwd: width above 256");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, 0, "gcn_aggregate_max_bwd", &query));
+  if (query) return GCN_OK;
+  if (g->n > 0 && w > 0 && (!d_dP || !d_arg || !d_dM))
+    return fail(GCN_E_INVALID, "gcn_aggregate_max_bwd: NULL buffer");
+  return launch_aggregate_max_bwd(graph_agg(g, w, d_dP, ldd, d_dM, ldo), g->nnz, d_arg, ldarg, d_mask, ldmask,
+                                  d_dM, ldo, stream);
 }
 
 gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_A, int64_t lda,

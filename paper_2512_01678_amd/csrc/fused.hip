@@ -121,6 +121,11 @@ __global__ void __launch_bounds__(256) k_agg_gemm(FusedArgs f) {
         }
       } else {
         acc = accumulate<LANES, 4>(p, beg, end, L, f.slots, cok, first);
+        const float sc = row_scale(p, row);
+        acc.x *= sc;
+        acc.y *= sc;
+        acc.z *= sc;
+        acc.w *= sc;
         if (cok && L.slot == 0) {
           if (cfull) {
             *reinterpret_cast<float4*>(prow) = acc;

@@ -67,12 +67,20 @@ struct ProfScope {
 // launchers (each validates nothing: callers in api.hip validate first)
 // ---------------------------------------------------------------------------
 enum AggEpi { AGG_NONE = 0, AGG_RELU = 1, AGG_MASK = 2, AGG_SOFTMAX = 3 };
+// Entry weights of a linear aggregation over the rows of a compressed matrix:
+//   AGG_W_VAL      val[e] (A_hat, or the values of X)
+//   AGG_W_ONE      1                      (sum over the row: A + I)
+//   AGG_W_ROWMEAN  1, the row sum times 1 / deg[u]  (mean: D^-1 (A + I))
+//   AGG_W_COLMEAN  1 / deg[col[e]]        (transpose of the mean: (A + I) D^-1)
+enum AggWeight { AGG_W_VAL = 0, AGG_W_ONE = 1, AGG_W_ROWMEAN = 2, AGG_W_COLMEAN = 3 };
 
 struct AggParams {
   int32_t n;               // output rows
   const int64_t* row_ptr;  // n + 1
   const int32_t* col;      // neighbours / column indices
-  const float* val;        // entry values (A_hat, or X in CSR / CSC form)
+  const float* val;        // entry values (A_hat, or X in CSR / CSC form); kind AGG_W_VAL
+  int32_t kind;            // AggWeight: where an entry's weight comes from
+  const int32_t* deg;      // row lengths, for the mean kinds
   const float* M;          // gathered rows
   int64_t ldm;
   int32_t w;
@@ -99,6 +107,13 @@ inline bool has_split(const gcn_split* sp) { return sp && sp->rows && sp->n_long
 // Neighbour slices per row for slices of `lanes` lanes on a matrix with nnz entries over
 // `rows` rows (nnz < 0: unknown).
 int agg_slots(int lanes, int64_t nnz, int64_t rows);
+// Max aggregation over the graph rows (P, arg) and its gradient (aggmax.hip).
+gcn_status launch_aggregate_max(const AggParams& p, int64_t nnz, float* P, int64_t ldp, int32_t* arg,
+                                int64_t ldarg, hipStream_t s);
+gcn_status launch_aggregate_max_bwd(const AggParams& p, int64_t nnz, const int32_t* arg, int64_t ldarg,
+                                    const float* mask, int64_t ldmask, float* dM, int64_t ldo, hipStream_t s);
+// Identity operator in CSR form: row_ptr[i] = i, col[i] = i.
+gcn_status launch_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col, hipStream_t s);
 // Only the long rows of a split plan (chunk sums, then their combination), no epilogue.
 gcn_status launch_aggregate_long_rows(const AggParams& p, const gcn_split* split, void* ws, hipStream_t s);
 

@@ -27,6 +27,7 @@ OK, E_INVALID, E_RANGE, E_OVERFLOW, E_CAPACITY, E_HIP, E_UNSUPPORTED = 0, -1, -2
 DENSE, SPARSE = 0, 1
 ACT_NONE, ACT_RELU, ACT_SOFTMAX_CE = 0, 1, 2
 ORDER_AUTO, TRANSFORM_FIRST, AGGREGATE_FIRST = 0, 1, 2
+AGG_NORM, AGG_SUM, AGG_MEAN, AGG_MEAN_T, AGG_MAX = 0, 1, 2, 3, 4
 EPI_NONE, EPI_RELU, EPI_MASK = 0, 1, 2
 OP_NN, OP_NT, OP_TN = 0, 1, 2
 
@@ -63,7 +64,7 @@ class gcn_feature_info(C.Structure):
 
 class gcn_layer(C.Structure):
     _fields_ = [("f_in", i32), ("f_out", i32), ("ld_in", i64), ("ld_out", i64), ("act", i32),
-                ("order", i32), ("index", i32)]
+                ("order", i32), ("index", i32), ("agg", i32)]
 
 
 class gcn_model(C.Structure):
@@ -95,7 +96,11 @@ _SIG = {
                             P, P, P, P, P, P, C.POINTER(sz), P]),
     "gcn_epoch": (i32, [C.POINTER(gcn_model), C.POINTER(gcn_graph), P, C.POINTER(gcn_sparse_x), P, P,
                         P, C.POINTER(sz), P]),
-    "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i32, P, i64, P, i64, P, C.POINTER(sz), P]),
+    "gcn_aggregate": (i32, [C.POINTER(gcn_graph), i32, i32, P, i64, P, i32, P, i64, P, i64, P, C.POINTER(sz),
+                            P]),
+    "gcn_aggregate_max": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i64, P, i64, P, C.POINTER(sz), P]),
+    "gcn_aggregate_max_bwd": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i64, P, i64, P, i64, P, C.POINTER(sz),
+                                    P]),
     "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
     "gcn_spmm": (i32, [i64, i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
@@ -264,12 +269,31 @@ def feature_stats(X: torch.Tensor, tau=(4, 5), force_mode=-1, materialize=None, 
 
 
 def aggregate(g: DeviceGraph, M: torch.Tensor, out: torch.Tensor, bias=None, epi=EPI_NONE, mask=None,
-              ws: _Workspace | None = None, stream=None):
+              ws: _Workspace | None = None, stream=None, agg=AGG_NORM):
     w = M.shape[1]
-    _run_ws(_lib.gcn_aggregate, (C.byref(g.c), w, _ptr(M), _ld(M), _ptr(bias), epi, _ptr(mask),
+    _run_ws(_lib.gcn_aggregate, (C.byref(g.c), agg, w, _ptr(M), _ld(M), _ptr(bias), epi, _ptr(mask),
                                  _ld(mask) if mask is not None else 0, _ptr(out), _ld(out)),
             (P(_stream(stream)),), "gcn_aggregate", ws, out.device)
     return out
+
+
+def aggregate_max(g: DeviceGraph, M: torch.Tensor, out: torch.Tensor, arg: torch.Tensor, stream=None):
+    """out = max over each row of A + I of M's rows, arg = the first maximiser (int32)."""
+    w = M.shape[1]
+    _run_ws(_lib.gcn_aggregate_max,
+            (C.byref(g.c), w, _ptr(M), _ld(M), _ptr(out), _ld(out), _ptr(arg), _ld(arg)),
+            (P(_stream(stream)),), "gcn_aggregate_max", None, M.device)
+    return out
+
+
+def aggregate_max_bwd(g: DeviceGraph, dP: torch.Tensor, arg: torch.Tensor, dM: torch.Tensor, mask=None,
+                      stream=None):
+    """dM[u] = sum over u's row of dP[v] where arg[v] == u (times 1[mask > 0])."""
+    w = dP.shape[1]
+    _run_ws(_lib.gcn_aggregate_max_bwd, (C.byref(g.c), w, _ptr(dP), _ld(dP), _ptr(arg), _ld(arg), _ptr(mask),
+                                         _ld(mask) if mask is not None else 0, _ptr(dM), _ld(dM)),
+            (P(_stream(stream)),), "gcn_aggregate_max_bwd", None, dP.device)
+    return dM
 
 
 def gemm(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, ws: _Workspace | None = None, stream=None):
@@ -310,13 +334,22 @@ def adam(params, grads, ms, vs, step, lr=0.01, b1=0.9, b2=0.999, eps=1e-8, strea
     _check(_lib.gcn_adam(arr, len(params), step, lr, b1, b2, eps, P(_stream(stream))), "gcn_adam")
 
 
-def layer_order(f_in, f_out, index, act, x_sparse=False, order=ORDER_AUTO):
-    L = gcn_layer(f_in, f_out, pitch(f_in), pitch(f_out), act, order, index)
+def layer_order(f_in, f_out, index, act, x_sparse=False, order=ORDER_AUTO, agg=AGG_NORM):
+    L = gcn_layer(f_in, f_out, pitch(f_in), pitch(f_out), act, order, index, agg)
     return _lib.gcn_layer_order(C.byref(L), int(x_sparse))
 
 
-def make_layer(f_in, f_out, ld_in, ld_out, act, index, order=ORDER_AUTO):
-    return gcn_layer(f_in, f_out, ld_in, ld_out, act, order, index)
+def make_layer(f_in, f_out, ld_in, ld_out, act, index, order=ORDER_AUTO, agg=AGG_NORM):
+    return gcn_layer(f_in, f_out, ld_in, ld_out, act, order, index, agg)
+
+
+def saved_buffer(n, f_in, ld_in, agg, device="cuda"):
+    """The d_saved buffer of an aggregate-first layer: n x f_in (pitch ld_in) fp32, and for a
+    max layer the n x ld_in int32 maximisers after it.  Returns (buffer view, argmax view)."""
+    rows = 2 * n if agg == AGG_MAX else n
+    buf = torch.zeros((rows, ld_in), dtype=torch.float32, device=device)
+    arg = buf[n:].view(torch.int32)[:, :f_in] if agg == AGG_MAX else None
+    return buf[:n, :f_in], arg
 
 
 def layer_fwd(g: DeviceGraph, L: gcn_layer, Hin, x: SparseFeatures | None, W, b, Hout, saved=None,
@@ -350,7 +383,7 @@ class Model:
     """
 
     def __init__(self, n, widths, Ws, bs, device="cuda", x_sparse=False, ld_x=None, lr=0.01,
-                 beta1=0.9, beta2=0.999, eps=1e-8, orders=None, device_step=False):
+                 beta1=0.9, beta2=0.999, eps=1e-8, orders=None, device_step=False, aggs=None):
         self.n = n
         self.widths = tuple(widths)
         L = len(widths) - 1
@@ -366,7 +399,8 @@ class Model:
             ld_out = pitch(fo)
             act = ACT_SOFTMAX_CE if l == L - 1 else ACT_RELU
             order = orders[l] if orders is not None else ORDER_AUTO
-            self.layers[l] = gcn_layer(fi, fo, ld_in, ld_out, act, order, l)
+            agg = aggs[l] if aggs is not None else AGG_NORM
+            self.layers[l] = gcn_layer(fi, fo, ld_in, ld_out, act, order, l, agg)
             self.W.append(torch.as_tensor(Ws[l], dtype=torch.float32).to(dev).contiguous())
             self.b.append(torch.as_tensor(bs[l], dtype=torch.float32).to(dev).contiguous())
             self.dW.append(torch.zeros_like(self.W[-1]))
@@ -380,7 +414,7 @@ class Model:
                 self.act.append(padded(n, fo, dev))
             resolved = _lib.gcn_layer_order(C.byref(self.layers[l]), int(x_sparse and l == 0))
             if resolved == AGGREGATE_FIRST:
-                self.saved.append(torch.zeros((n, ld_in), dtype=torch.float32, device=dev)[:, :fi])
+                self.saved.append(saved_buffer(n, fi, ld_in, agg, dev)[0])
             else:
                 self.saved.append(None)
         self.loss = torch.zeros(1, dtype=torch.float32, device=dev)

@@ -70,7 +70,7 @@ def test_status_strings(G):
     assert L.gcn_status_string(0) == b"GCN_OK"
     assert L.gcn_status_string(-4) == b"GCN_E_CAPACITY"
     assert L.gcn_status_string(-99) == b"GCN_E_UNKNOWN"
-    assert L.gcn_version() >= 2
+    assert L.gcn_version() >= 3
 
 
 def test_host_validation_rejects_bad_calls(G):
@@ -100,22 +100,22 @@ def test_host_validation_rejects_bad_calls(G):
     nb2 = G.sz(1 << 20)
     assert L.gcn_gemm(G.OP_NN, 4, 4, 4, None, 4, 1, 4, 1, 4, None, 0, None, 0, 1, C.byref(nb2), None) == G.E_INVALID
     # aggregate: NULL graph, mask epilogue without mask
-    assert L.gcn_aggregate(None, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_aggregate(None, 0, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
     g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1)
-    assert L.gcn_aggregate(C.byref(g2), 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None, C.byref(nb),
+    assert L.gcn_aggregate(C.byref(g2), 0, 4, 1, 4, None, G.EPI_MASK, None, 0, 1, 4, None, C.byref(nb),
                            None) == G.E_INVALID
-    assert L.gcn_aggregate(C.byref(g2), 4, 1, 3, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(g2), 0, 4, 1, 3, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
     # the entries of A_hat are required
     noval = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, None)
-    assert L.gcn_aggregate(C.byref(noval), 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(noval), 0, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb), None) == G.E_INVALID
     assert L.gcn_build_csr(10, 5, 1, 1, C.byref(noval), 1, C.byref(G.sz(1 << 20)), None) == G.E_INVALID
     # a split plan with long rows needs its chunk sums in the workspace
     sp = G.gcn_split(3, 50, 64, 1, 1, 1, None)
     g3 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1, sp)
-    assert L.gcn_aggregate(C.byref(g3), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.OK
+    assert L.gcn_aggregate(C.byref(g3), 0, 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.OK
     assert nb.value == 50 * 40 * 4
     bad = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1, G.gcn_split(3, 50, 64, 1, None, 1, None))
-    assert L.gcn_aggregate(C.byref(bad), 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_aggregate(C.byref(bad), 0, 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.E_INVALID
     # spmm: bad pitch
     assert L.gcn_spmm(10, 20, 1, 1, 1, 5, 8, 1, 7, 1, 8, None, None, C.byref(nb), None) == G.E_INVALID
     # adam: step 0, too many tensors
@@ -151,6 +151,35 @@ def test_layer_validation(G):
     assert L.gcn_layer_fwd(C.byref(g), C.byref(lay), 1, None, 1, 1, 1, None, None, None, None, None,
                            C.byref(nb), None) == G.OK
     assert nb.value >= 10 * 4 * 4
+    # aggregators: unknown kind, max forced transform-first, max too wide, max on sparse X
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(G.gcn_layer(8, 4, 8, 4, G.ACT_RELU, G.ORDER_AUTO, 1, 9)), 1, None,
+                           1, 1, 1, 1, None, None, None, None, C.byref(nb), None) == G.E_INVALID
+    mx_tf = G.gcn_layer(8, 4, 8, 4, G.ACT_RELU, G.TRANSFORM_FIRST, 1, G.AGG_MAX)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(mx_tf), 1, None, 1, 1, 1, 1, None, None, None, None,
+                           C.byref(nb), None) == G.E_INVALID
+    mx_wide = G.gcn_layer(300, 4, 300, 4, G.ACT_RELU, G.ORDER_AUTO, 1, G.AGG_MAX)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(mx_wide), 1, None, 1, 1, 1, 1, None, None, None, None,
+                           C.byref(nb), None) == G.E_UNSUPPORTED
+    mx = G.gcn_layer(8, 4, 8, 4, G.ACT_RELU, G.ORDER_AUTO, 0, G.AGG_MAX)
+    assert L.gcn_layer_order(C.byref(mx), 0) == G.AGGREGATE_FIRST
+    assert L.gcn_layer_order(C.byref(mx), 1) == G.AGGREGATE_FIRST
+    sxm = G.gcn_sparse_x(10, 8, 5, 1, 1, 1, 1, 1, 1)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(mx), None, C.byref(sxm), 1, 1, 1, 1, None, None, None, None,
+                           C.byref(nb), None) == G.E_UNSUPPORTED
+    # a max loss layer is allowed (aggregate-first with the softmax epilogue)
+    mx_sm = G.gcn_layer(8, 4, 8, 4, G.ACT_SOFTMAX_CE, G.ORDER_AUTO, 1, G.AGG_MAX)
+    assert L.gcn_layer_fwd(C.byref(g), C.byref(mx_sm), 1, None, 1, 1, 1, 1, 1, 1, None, None,
+                           C.byref(nb), None) == G.OK
+    # gcn_aggregate takes the linear aggregators only; the max one has its own calls
+    g2 = G.gcn_graph(10, 20, 20, 1, 1, 1, 1, 1)
+    assert L.gcn_aggregate(C.byref(g2), G.AGG_MAX, 4, 1, 4, None, 0, None, 0, 1, 4, None, C.byref(nb),
+                           None) == G.E_INVALID
+    nb.value = 99
+    assert L.gcn_aggregate_max(C.byref(g2), 4, 1, 4, 1, 4, 1, 4, None, C.byref(nb), None) == G.OK
+    assert nb.value == 0
+    assert L.gcn_aggregate_max(C.byref(g2), 300, 1, 300, 1, 300, 1, 300, None, C.byref(nb), None) == G.E_UNSUPPORTED
+    assert L.gcn_aggregate_max_bwd(C.byref(g2), 4, 1, 4, 1, 4, None, 0, 1, 3, None, C.byref(nb),
+                                   None) == G.E_INVALID
     # backward: sparse input cannot have an input gradient
     sx = G.gcn_sparse_x(10, 8, 5, 1, 1, 1, 1, 1, 1)
     assert L.gcn_layer_bwd(C.byref(g), C.byref(lay), 1, None, C.byref(sx), None, 1, 1, 1, 1, None,

@@ -431,6 +431,64 @@ def test_aggregate_first_layer_on_split_hubs(G, orc, hub_graph, fi, fo):
     assert_mag_close(host(out), np.maximum(Z, 0), mag, f"split hubs: AF {fi}->{fo}")
 
 
+# ---------------------------------------------------------------------------
+# other aggregators: sum, mean and its transpose, max (forward and gradient)
+# ---------------------------------------------------------------------------
+
+AGG_CODE = {"sum": 1, "mean": 2, "mean_t": 3}
+
+
+@pytest.mark.parametrize("kind", ["sum", "mean", "mean_t"])
+@pytest.mark.parametrize("w", [7, 40, 256])
+def test_linear_aggregators_on_split_hubs(G, orc, hub_graph, kind, w):
+    og, dg = hub_graph
+    rng = np.random.default_rng(w + 7)
+    n = og.n
+    M = rng.standard_normal((n, w)).astype(np.float32)
+    b = rng.standard_normal(w).astype(np.float32)
+    mask = rng.standard_normal((n, w)).astype(np.float32)
+    ld = G.pitch(w)
+    Md = pitched(M, ld)
+    Zd = pitched(np.zeros((n, w), np.float32), ld)
+    Z, mag = orc.aggregate(og, M, b, want_mag=True, kind=kind)
+    for epi in (G.EPI_NONE, G.EPI_RELU, G.EPI_MASK):
+        G.aggregate(dg, Md, Zd, bias=dev(b), epi=epi, mask=pitched(mask, ld) if epi == G.EPI_MASK else None,
+                    agg=AGG_CODE[kind])
+        want = Z if epi == G.EPI_NONE else (np.maximum(Z, 0) if epi == G.EPI_RELU else Z * (mask > 0))
+        assert_mag_close(host(Zd), want, mag, f"{kind} aggregate w={w} epi={epi}")
+
+
+@pytest.mark.parametrize("w,ld", [(7, 7), (7, 8), (40, 40), (128, 128), (256, 256), (41, 41)])
+def test_max_aggregation_bit_exact_with_ties(G, orc, hub_graph, w, ld):
+    """Max and first maximiser are exact in fp32: equal to the oracle bit for bit, also on
+    rows of small integers (many ties) and on the hub rows (walked by one lane group)."""
+    og, dg = hub_graph
+    n = og.n
+    rng = np.random.default_rng(w * 3 + ld)
+    M = rng.integers(-3, 4, (n, w)).astype(np.float32)
+    M[::7] = rng.standard_normal((M[::7].shape)).astype(np.float32)
+    Pd = pitched(np.zeros((n, w), np.float32), ld)
+    argd = torch.zeros((n, ld), dtype=torch.int32, device="cuda")[:, :w]
+    G.aggregate_max(dg, pitched(M, ld), Pd, argd)
+    P, arg = orc.aggregate_max(og, M)
+    np.testing.assert_array_equal(host(Pd), P.astype(np.float32))
+    np.testing.assert_array_equal(host(argd), arg)
+    # gradient: the gather over the symmetric rows against the oracle's scatter
+    dP = rng.standard_normal((n, w)).astype(np.float32)
+    mask = rng.standard_normal((n, w)).astype(np.float32)
+    dMd = pitched(np.zeros((n, w), np.float32), ld)
+    for use_mask in (False, True):
+        G.aggregate_max_bwd(dg, pitched(dP, ld), argd, dMd, mask=pitched(mask, ld) if use_mask else None)
+        want = orc.aggregate_max_backward(og, dP, arg)
+        mag = orc.aggregate_max_backward(og, np.abs(dP), arg)
+        if use_mask:
+            want, mag = want * (mask > 0), mag * (mask > 0)
+        assert_mag_close(host(dMd), want, mag, f"max gradient w={w} mask={use_mask}")
+    first = host(dMd).copy()
+    G.aggregate_max_bwd(dg, pitched(dP, ld), argd, dMd, mask=pitched(mask, ld))
+    np.testing.assert_array_equal(host(dMd), first)  # fixed order
+
+
 def test_sparse_backward_long_columns(G, orc):
     """X with few, dense columns: every CSC column is long and goes through chunks
     processed chunk-index-major."""

@@ -192,7 +192,10 @@ def snapshot(m):
     return {k: [host(t) for t in getattr(m, k)] for k in ("W", "b", "mW", "vW", "mb", "vb")}
 
 
-def run_epochs(G, orc, p, epochs, sparse):
+AGGS = {"gcn": 0, "sum": 1, "mean": 2, "max": 4}
+
+
+def run_epochs(G, orc, p, epochs, sparse, aggs=None):
     """Each epoch: the oracle starts from the GPU's own pre-epoch parameters and Adam
     state, so every epoch is a well-conditioned comparison (Adam's first steps move
     each weight by about lr * sign(g), which would amplify rounding in g if the two
@@ -203,14 +206,15 @@ def run_epochs(G, orc, p, epochs, sparse):
     if sparse:
         info, sx = G.feature_stats(Xd)
         assert info["mode"] == G.SPARSE
-    m = G.Model(n, p.wl.widths, p.Ws, p.bs, x_sparse=sparse, ld_x=p.wl.f)
+    m = G.Model(n, p.wl.widths, p.Ws, p.bs, x_sparse=sparse, ld_x=p.wl.f,
+                aggs=[AGGS[a] for a in aggs] if aggs else None)
     yd = dev(p.y)
     osx = orc.SparseX(p.X) if sparse else None
     for t in range(1, epochs + 1):
         st = snapshot(m)
         m.epoch(p.dg, X=None if sparse else Xd, x=sx, labels=yd)
         out = orc.epoch(p.og, p.X, p.y, st["W"], st["b"], st["mW"], st["vW"], st["mb"], st["vb"], t,
-                        sparse=osx)
+                        sparse=osx, aggs=list(aggs) if aggs else None)
         tag = f"{p.wl.name} epoch {t}"
         assert host(m.loss)[0] == pytest.approx(out["loss"], rel=1e-4), tag
         for l in range(m.L):
@@ -240,6 +244,73 @@ def test_epochs_sparse_path_cora_like(G, orc, cora):
 def test_epochs_dense_path_aggregate_first(G, orc, small):
     m = run_epochs(G, orc, small, 2, sparse=False)
     assert m.orders()[0] == G.AGGREGATE_FIRST and m.orders()[1] == G.TRANSFORM_FIRST
+
+
+@pytest.fixture(scope="module")
+def tiny(G, orc):
+    wl = gs.scaled(gs.WORKLOADS["arxiv_like"], 3000, 15000, name="arxiv_like_tiny")
+    wl = gs.Workload(wl.name, wl.n, wl.graph, wl.e_und, (48, 24, 16, 8), wl.features, wl.density)
+    return Problem(G, orc, wl)
+
+
+@pytest.mark.parametrize("aggs", [("sum", "mean", "gcn"), ("max", "sum", "mean"), ("mean", "max", "max")])
+def test_epochs_other_aggregators(G, orc, tiny, aggs):
+    """Whole epochs with sum, mean and max layers (the max loss layer goes through the
+    softmax epilogue after its GEMM) against the oracle run from X alone."""
+    m = run_epochs(G, orc, tiny, 2, sparse=False, aggs=aggs)
+    for l, a in enumerate(aggs):
+        if a == "max":
+            assert m.orders()[l] == G.AGGREGATE_FIRST
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "max"])
+@pytest.mark.parametrize("order", ["TF", "AF"])
+def test_aggregator_layer_unit_parity(G, orc, small, agg, order):
+    """One hidden layer forward and backward with the GPU's own inputs fed to the oracle."""
+    if agg == "max" and order == "TF":
+        pytest.skip("a max layer is always aggregate-first")
+    og, dg, n = small.og, small.dg, small.wl.n
+    fi, fo = 48, 64
+    rng = np.random.default_rng(fi + fo + len(agg))
+    H = np.maximum(rng.standard_normal((n, fi)), 0).astype(np.float32)
+    W = (rng.standard_normal((fi, fo)) / np.sqrt(fi)).astype(np.float32)
+    b = (rng.standard_normal(fo) * 0.1).astype(np.float32)
+    code = AGGS[agg]
+    L = G.make_layer(fi, fo, G.pitch(fi), G.pitch(fo), G.ACT_RELU, 1,
+                     G.TRANSFORM_FIRST if order == "TF" else G.AGGREGATE_FIRST, agg=code)
+    Hd = pad(G, H)
+    out = G.padded(n, fo)
+    saved, arg = G.saved_buffer(n, fi, G.pitch(fi), code) if order == "AF" else (None, None)
+    G.layer_fwd(dg, L, Hd, None, dev(W), dev(b), out, saved=saved)
+    if agg == "max":
+        P, oarg = orc.aggregate_max(og, H)
+        np.testing.assert_array_equal(host(saved), P)
+        np.testing.assert_array_equal(arg.cpu().numpy(), oarg)
+        Z, mag = orc.matmul(P, W, want_mag=True)
+        Z, mag = Z + b, mag + np.abs(b)
+    else:
+        Z = orc.aggregate(og, orc.matmul(H, W), b, kind=agg)
+        mag = orc.aggregate(og, orc.matmul(np.abs(H), np.abs(W)), np.abs(b), kind=agg)
+    assert_mag_close(host(out), np.maximum(Z, 0), mag, f"{agg} {order} forward")
+    Gr = (rng.standard_normal((n, fo)) / n).astype(np.float32)
+    dW = torch.zeros((fi, fo), device="cuda")
+    db = torch.zeros(fo, device="cuda")
+    Gprev = G.padded(n, fi)
+    G.layer_bwd(dg, L, pad(G, Gr), Hd, None, saved, dev(W), dW, db, Gprev)
+    T, Tm = orc.matmul(Gr, W.T, want_mag=True)
+    if agg == "max":
+        assert_mag_close(host(dW), orc.matmul(P.T, Gr), orc.matmul(np.abs(P).T, np.abs(Gr)), "max dW")
+        want = orc.aggregate_max_backward(og, T, oarg) * (H > 0)
+        wmag = orc.aggregate_max_backward(og, Tm, oarg) * (H > 0)
+    else:
+        tk = orc.TRANSPOSE[agg]
+        Q = orc.aggregate(og, Gr, kind=tk)
+        Qm = orc.aggregate(og, np.abs(Gr), kind=tk)
+        assert_mag_close(host(dW), orc.matmul(H.T, Q), orc.matmul(np.abs(H).T, Qm), f"{agg} dW")
+        want = orc.matmul(Q, W.T) * (H > 0)
+        wmag = orc.matmul(Qm, np.abs(W).T) * (H > 0)
+    assert_mag_close(host(db), Gr.astype(np.float64).sum(0), np.abs(Gr).astype(np.float64).sum(0), f"{agg} db")
+    assert_mag_close(host(Gprev), want, wmag, f"{agg} {order} G_prev")
 
 
 def test_epochs_forced_dense_on_sparse_features(G, orc, cora):
