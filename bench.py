@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--workload", default="arxiv_like")
     ap.add_argument("--tau", default="4/5", help="sparse-path threshold tau as num/den")
     ap.add_argument("--force-mode", default="auto", choices=["auto", "dense", "sparse"])
+    ap.add_argument("--agg", default="gcn", choices=["gcn", "sum", "mean", "max"],
+                    help="aggregator of every layer (Section III-A); gcn is the normalised A_hat")
     ap.add_argument("--cpu-baseline", default="auto", choices=["auto", "off"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU work budget for the oracle leg")
     ap.add_argument("--no-profile", action="store_true", help="no per-launch events (pure epoch timing)")
@@ -184,7 +186,11 @@ def main():
         torch.cuda.empty_cache()
     setup_peak = torch.cuda.max_memory_allocated(dev)
     torch.cuda.reset_peak_memory_stats(dev)
-    m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x, device_step=args.graph)
+    agg = {"gcn": G.AGG_NORM, "sum": G.AGG_SUM, "mean": G.AGG_MEAN, "max": G.AGG_MAX}[args.agg]
+    if agg == G.AGG_MAX and sparse:
+        sys.exit("bench.py: the max aggregator needs dense input features (use --force-mode dense)")
+    m = G.Model(wl.n, wl.widths, Ws, bs, device=dev, x_sparse=sparse, ld_x=ld_x, device_step=args.graph,
+                aggs=[agg] * (len(wl.widths) - 1))
     Xin = None if sparse else Xv
     for _ in range(args.warmup):
         m.epoch(g, X=Xin, x=sx, labels=yd)
@@ -238,6 +244,14 @@ def main():
         if name.startswith("aggregate_w"):
             by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
             k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+        elif name.startswith("aggmax_bwd_w"):  # gathers dP and maximisers, mask and output rows
+            w = f["width"]
+            by = 8 * g.nnz * w + 4 * g.nnz + 8 * (f["rows"] + 1) + 8 * f["rows"] * w
+            k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+        elif name.startswith("aggmax_w"):  # gathers, indices, offsets, maxima and maximisers out
+            w = f["width"]
+            by = 4 * g.nnz * w + 4 * g.nnz + 8 * (f["rows"] + 1) + 8 * f["rows"] * w
+            k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
         elif name.startswith("agg_gemm_"):
             fi, fo = (int(v) for v in name.split("_")[2].split("x"))
             by = alg_bytes_aggregate(g.nnz, f["rows"], fi) + 4 * f["rows"] * fo
@@ -286,6 +300,8 @@ def main():
     cpu = None
     if args.cpu_baseline == "auto" and X is None:
         print("[bench] no host copy of X for this workload: cpu_baseline skipped", file=sys.stderr, flush=True)
+    elif args.cpu_baseline == "auto" and args.agg != "gcn":
+        print("[bench] cpu_baseline is timed for the gcn aggregator only", file=sys.stderr, flush=True)
     elif args.cpu_baseline == "auto":
         print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
         cpu = cpu_baseline(wl, s, d, X, y, Ws, bs, sparse, args.cpu_seconds)
@@ -298,7 +314,7 @@ def main():
         "config": {"workload": wl.name, "nodes": wl.n, "nnz_A_plus_I": g.nnz, "widths": list(wl.widths),
                    "feature_path": "sparse" if sparse else "dense", "sparsity": round(info["sparsity"], 6),
                    "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
-                   "per_launch_events": profile, "hip_graph": bool(args.graph),
+                   "aggregator": args.agg, "per_launch_events": profile, "hip_graph": bool(args.graph),
                    "gemm_mode": "fp32 MFMA" if os.environ.get("GCN_GEMM_MODE") == "fp32"
                    else "fp32 via exact 3-way bf16 split, 6 bf16 MFMA products"},
         "roofline": roofline, "cpu_baseline": cpu, "spmm": spmm, "memory": memory, "kernels": kernels,
