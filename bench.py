@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--workload", default="arxiv_like")
     ap.add_argument("--tau", default="4/5", help="sparse-path threshold tau as num/den")
     ap.add_argument("--force-mode", default="auto", choices=["auto", "dense", "sparse"])
+    ap.add_argument("--csc", default="on", choices=["on", "off"],
+                    help="off: no X_csc view; the sparse backward X^T Q uses atomic adds from X_csr")
     ap.add_argument("--agg", default="gcn", choices=["gcn", "sum", "mean", "max"],
                     help="aggregator of every layer (Section III-A); gcn is the normalised A_hat")
     ap.add_argument("--cpu-baseline", default="auto", choices=["auto", "off"])
@@ -174,7 +176,7 @@ def main():
     tau = tuple(int(v) for v in args.tau.split("/"))
     force = {"auto": -1, "dense": G.DENSE, "sparse": G.SPARSE}[args.force_mode]
     t0 = time.perf_counter()
-    info, sx = G.feature_stats(Xv, tau=tau, force_mode=force)
+    info, sx = G.feature_stats(Xv, tau=tau, force_mode=force, csc=args.csc == "on")
     t_probe = time.perf_counter() - t0
     sparse = info["mode"] == G.SPARSE
     print(f"[bench] nnz(A+I)={g.nnz} csr {t_csr * 1e3:.1f} ms; probe s={info['sparsity']:.4f} -> "
@@ -289,8 +291,10 @@ def main():
     # on) against the O(N F) model: nothing may scale with nnz times a feature width
     graph_bytes = 8 * (wl.n + 1) + 8 * g.col_idx.numel() + 8 * wl.n  # offsets, indices + values, deg + dinv
     x_bytes = 0 if sparse else 4 * wl.n * ld_x
-    if sparse:  # X_csr and X_csc: offsets, indices, values
-        x_bytes = 8 * (wl.n + 1) + 8 * (wl.f + 1) + 16 * sx.col.numel()
+    if sparse:  # X_csr (and X_csc): offsets, indices, values
+        x_bytes = 8 * (wl.n + 1) + 8 * sx.col.numel()
+        if sx.col_ptr is not None:
+            x_bytes += 8 * (wl.f + 1) + 8 * sx.col.numel()
     train_peak = torch.cuda.max_memory_allocated(dev)
     memory = {"train_peak_bytes": train_peak, "setup_peak_bytes": setup_peak, "graph_bytes": graph_bytes,
               "x_bytes": x_bytes,
@@ -314,7 +318,8 @@ def main():
         "config": {"workload": wl.name, "nodes": wl.n, "nnz_A_plus_I": g.nnz, "widths": list(wl.widths),
                    "feature_path": "sparse" if sparse else "dense", "sparsity": round(info["sparsity"], 6),
                    "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
-                   "aggregator": args.agg, "per_launch_events": profile, "hip_graph": bool(args.graph),
+                   "aggregator": args.agg, "x_csc": sparse and args.csc == "on",
+                   "per_launch_events": profile, "hip_graph": bool(args.graph),
                    "gemm_mode": "fp32 MFMA" if os.environ.get("GCN_GEMM_MODE") == "fp32"
                    else "fp32 via exact 3-way bf16 split, 6 bf16 MFMA products"},
         "roofline": roofline, "cpu_baseline": cpu, "spmm": spmm, "memory": memory, "kernels": kernels,

@@ -237,7 +237,10 @@ gcn_status gcn_layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* d_
  * d_G = dLoss/dZ (n x f_out, pitch ld_out).  Writes d_dW = dLoss/dW (f_in x
  * f_out, pitch f_out) and d_db = sum_i G[i,:] (f_out).  With Q = S^T G (A_hat
  * and A + I are symmetric; the mean's transpose is (A + I) D^-1): dW = H_in^T Q,
- * or X^T Q via X_csc on the sparse path.  When d_Gprev != NULL (layers above the
+ * or X^T Q on the sparse path: gathered through X_csc when x has the CSC view, else
+ * (x->col_ptr == NULL, which saves the CSC memory) by atomic adds from the rows of
+ * X_csr, the implicit transpose of Section IV-D, whose rounding order is not fixed
+ * (results vary within fp32 rounding from run to run; f_out <= 256).  When d_Gprev != NULL (layers above the
  * first) it receives the gradient of the previous layer's pre-activation:
  * (Q W^T) * 1[H_in > 0] (n x f_in, pitch ld_in).  Max layers: dW = P^T G with the
  * saved maxima P, and G_prev routes (G W^T)[u,c] to the saved maximiser of (u, c).

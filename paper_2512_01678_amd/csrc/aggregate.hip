@@ -278,12 +278,71 @@ gcn_status launch_aggregate_long_rows(const AggParams& p, const gcn_split* split
 int agg_slots(int lanes, int64_t nnz, int64_t rows) { return pick_slots(lanes, nnz, rows); }
 
 namespace {
+// Implicit transpose with atomics (Section IV-D, the CUDA backend's sparse backward):
+// C[idx[e], :] += val[e] * B[i, :] for every entry e of compressed row i.  One lane
+// group per row reads B's row once and adds it, scaled, into the output row of each
+// entry.  Floating-point atomic adds make the order of the additions, and so the
+// rounding, vary from run to run.
+template <int LANES>
+__global__ void __launch_bounds__(256) k_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx,
+                                                       const float* val, const float* B, int64_t ldb, int32_t w,
+                                                       float* C, int64_t ldc) {
+  const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / LANES;
+  const int lane = threadIdx.x % LANES;
+  if (row >= nrows) return;
+  const int c0 = 4 * lane;
+  if (c0 >= w) return;
+  const float* b = B + row * ldb + c0;
+  float x[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) x[q] = c0 + q < w ? b[q] : 0.f;
+  for (int64_t e = ptr[row]; e < ptr[row + 1]; ++e) {
+    const float v = val[e];
+    float* c = C + (int64_t)idx[e] * ldc + c0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (c0 + q < w) atomicAdd(c + q, v * x[q]);
+  }
+}
+
+__global__ void __launch_bounds__(256) k_zero_rows(int64_t rows, int32_t w, float* C, int64_t ldc) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < rows * (int64_t)w) C[(i / w) * ldc + i % w] = 0.f;
+}
+
 __global__ void k_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i <= n) row_ptr[i] = i;
   if (i < n) col[i] = (int32_t)i;
 }
 }  // namespace
+
+gcn_status launch_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx, const float* val,
+                                const float* B, int64_t ldb, int32_t w, int64_t out_rows, float* C, int64_t ldc,
+                                int64_t nnz, hipStream_t s) {
+  if (out_rows > 0 && w > 0) {
+    hipLaunchKernelGGL(k_zero_rows, dim3((unsigned)ceil_div(out_rows * w, 256)), dim3(256), 0, s, out_rows, w, C,
+                       ldc);
+    GCN_TRY(check_launch("zero rows"));
+  }
+  if (nrows == 0 || w == 0) return GCN_OK;
+  char name[64];
+  snprintf(name, sizeof name, "spmm_t_atomic_w%d", w);
+  ProfScope prof(name, w, nrows, nnz, s);
+  if (w <= 64) {
+    hipLaunchKernelGGL(k_spmm_t_atomic<16>, dim3((unsigned)ceil_div(nrows * 16, 256)), dim3(256), 0, s, nrows,
+                       ptr, idx, val, B, ldb, w, C, ldc);
+  } else if (w <= 128) {
+    hipLaunchKernelGGL(k_spmm_t_atomic<32>, dim3((unsigned)ceil_div(nrows * 32, 256)), dim3(256), 0, s, nrows,
+                       ptr, idx, val, B, ldb, w, C, ldc);
+  } else if (w <= 256) {
+    hipLaunchKernelGGL(k_spmm_t_atomic<64>, dim3((unsigned)ceil_div(nrows * 64, 256)), dim3(256), 0, s, nrows,
+                       ptr, idx, val, B, ldb, w, C, ldc);
+  } else {
+    return fail(GCN_E_UNSUPPORTED, "atomic transpose product: width above 256");
+  }
+  return check_launch("atomic transpose product");
+}
 
 gcn_status launch_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col, hipStream_t s) {
   hipLaunchKernelGGL(k_identity_csr, dim3((unsigned)ceil_div((int64_t)n + 1, 256)), dim3(256), 0, s, n, row_ptr,

@@ -313,12 +313,15 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   GemmParams dw = gemm(L->f_in, L->f_out, n, Hin, L->ld_in, true, Q, ldq, false, dW, L->f_out);
   void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(dw));
   const size_t agg_need = std::max(aggregate_workspace(&g->split, L->f_out),
-                                   x ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
+                                   x && x->col_ptr ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
   void* aws = a.take<char>((int64_t)agg_need);
   if (!run) return GCN_OK;
   GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq, agg_transpose(L->agg)), g->nnz,
                            &g->split, aws, s));
-  if (x) {
+  if (x && !x->col_ptr) {
+    // no CSC view: dW = X^T Q by atomic adds from the CSR rows (Section IV-D)
+    GCN_TRY(launch_spmm_t_atomic(n, x->row_ptr, x->col, x->val, Q, ldq, L->f_out, x->f, dW, L->f_out, x->nnz, s));
+  } else if (x) {
     AggParams p{};
     p.n = x->f;
     p.row_ptr = x->col_ptr;
@@ -372,7 +375,9 @@ gcn_status validate_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, 
   GCN_TRY(check_layer(L, who));
   if (!G || !W || !dW || !db) return fail(GCN_E_INVALID, std::string(who) + ": G, W, dW and db are required");
   if (x) {
-    GCN_TRY(check_sparse(x, g, L, true, who));
+    GCN_TRY(check_sparse(x, g, L, false, who));  // without X_csc: the atomic implicit transpose
+    if (!x->col_ptr && L->f_out > 256)
+      return fail(GCN_E_UNSUPPORTED, std::string(who) + ": the atomic transpose product needs f_out <= 256");
     if (Gprev) return fail(GCN_E_INVALID, std::string(who) + ": no input gradient for sparse X");
   } else if (!Hin) {
     return fail(GCN_E_INVALID, std::string(who) + ": d_Hin is required for a dense input");
@@ -506,7 +511,6 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
         !m->mb[l] || !m->vb[l] || (l < L - 1 && !m->act[l]))
       return fail(GCN_E_INVALID, "gcn_epoch: a layer buffer is NULL");
   }
-  if (x && !x->col_ptr) return fail(GCN_E_INVALID, "gcn_epoch: the sparse path needs X_csc");
   // validate every layer call, then plan the workspace as the maximum over the layer calls
   size_t need = 0;
   for (int l = 0; l < L; ++l) {

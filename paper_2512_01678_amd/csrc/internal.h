@@ -112,6 +112,11 @@ gcn_status launch_aggregate_max(const AggParams& p, int64_t nnz, float* P, int64
                                 int64_t ldarg, hipStream_t s);
 gcn_status launch_aggregate_max_bwd(const AggParams& p, int64_t nnz, const int32_t* arg, int64_t ldarg,
                                     const float* mask, int64_t ldmask, float* dM, int64_t ldo, hipStream_t s);
+// C (out_rows x w) = X^T B from X's CSR rows with atomic adds (C is zeroed first);
+// non-deterministic rounding order.  w <= 256.
+gcn_status launch_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx, const float* val,
+                                const float* B, int64_t ldb, int32_t w, int64_t out_rows, float* C, int64_t ldc,
+                                int64_t nnz, hipStream_t s);
 // Identity operator in CSR form: row_ptr[i] = i, col[i] = i.
 gcn_status launch_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col, hipStream_t s);
 // Only the long rows of a split plan (chunk sums, then their combination), no epilogue.

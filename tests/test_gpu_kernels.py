@@ -489,6 +489,26 @@ def test_max_aggregation_bit_exact_with_ties(G, orc, hub_graph, w, ld):
     np.testing.assert_array_equal(host(dMd), first)  # fixed order
 
 
+def test_sparse_backward_atomic_transpose(G, orc):
+    """X^T Q from the CSR rows with atomic adds (no CSC view): within the fp32 bar of the
+    oracle; the rounding order may differ between runs, the values stay within it."""
+    n, f, w = 20000, 300, 40
+    X = gs.features_bernoulli(n, f, 0.05, seed=4, binary=False)
+    rng = np.random.default_rng(3)
+    Q = rng.standard_normal((n, w)).astype(np.float32)
+    info, sx = G.feature_stats(dev(X), force_mode=G.SPARSE, csc=False)
+    assert sx.col_ptr is None
+    L = G.make_layer(f, w, f, G.pitch(w), G.ACT_RELU, 0)
+    dW = torch.zeros((f, w), device="cuda")
+    db = torch.zeros(w, device="cuda")
+    g = G.build_csr(n, dev(np.zeros(0, np.int32)), dev(np.zeros(0, np.int32)))  # A + I = I: Q passes through
+    G.layer_bwd(g, L, pitched(Q, G.pitch(w)), None, sx, None, dev(np.zeros((f, w), np.float32)), dW, db, None)
+    rp, col, val = orc.dense_to_csr(X)
+    want = orc.matmul(X.T, Q)
+    mag = orc.matmul(np.abs(X).T, np.abs(Q))
+    assert_mag_close(host(dW), want, mag, "atomic X^T Q")
+
+
 def test_sparse_backward_long_columns(G, orc):
     """X with few, dense columns: every CSC column is long and goes through chunks
     processed chunk-index-major."""

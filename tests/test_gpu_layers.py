@@ -195,7 +195,7 @@ def snapshot(m):
 AGGS = {"gcn": 0, "sum": 1, "mean": 2, "max": 4}
 
 
-def run_epochs(G, orc, p, epochs, sparse, aggs=None):
+def run_epochs(G, orc, p, epochs, sparse, aggs=None, csc=True):
     """Each epoch: the oracle starts from the GPU's own pre-epoch parameters and Adam
     state, so every epoch is a well-conditioned comparison (Adam's first steps move
     each weight by about lr * sign(g), which would amplify rounding in g if the two
@@ -204,7 +204,7 @@ def run_epochs(G, orc, p, epochs, sparse, aggs=None):
     Xd = dev(p.X)
     sx = None
     if sparse:
-        info, sx = G.feature_stats(Xd)
+        info, sx = G.feature_stats(Xd, csc=csc)
         assert info["mode"] == G.SPARSE
     m = G.Model(n, p.wl.widths, p.Ws, p.bs, x_sparse=sparse, ld_x=p.wl.f,
                 aggs=[AGGS[a] for a in aggs] if aggs else None)
@@ -239,6 +239,12 @@ def run_epochs(G, orc, p, epochs, sparse, aggs=None):
 def test_epochs_sparse_path_cora_like(G, orc, cora):
     m = run_epochs(G, orc, cora, 3, sparse=True)
     assert m.step == 3
+
+
+def test_epochs_sparse_path_atomic_transpose(G, orc, cora):
+    """Sparse path without the CSC view: X^T Q by atomic adds from X_csr (Section IV-D)."""
+    m = run_epochs(G, orc, cora, 2, sparse=True, csc=False)
+    assert m.step == 2
 
 
 def test_epochs_dense_path_aggregate_first(G, orc, small):
