@@ -2,13 +2,13 @@
 // normalised aggregation followed by the dense transform of Algorithm 1):
 //   P = A_hat X          (kept: the backward pass needs dW = P^T G)
 //   H = act(P W + b)
-// A workgroup owns a block of kRows rows.  Its four wavefronts aggregate the rows
+// A workgroup owns a block of kRows rows.  Its eight wavefronts aggregate the rows
 // with the same lane-slice code and slice count as the standalone aggregation (so P
 // is bit-identical to it), prefetching each next row's offsets and first index chunk
 // during the current row's gathers; they write each P row to memory and split it
 // into three bf16 planes in LDS (the bf16x6 arithmetic of the dense products).  The
-// block's rows then meet W on the matrix cores: every wavefront owns 64 output
-// columns, one 32-column tile at a time, reads its A fragments from LDS and its W
+// block's rows then meet W on the matrix cores: every wavefront owns 32 output
+// columns of each 256-column chunk, reads its A fragments from LDS and its W
 // fragments (one step ahead) from planes of W that are split once per call and stay
 // in L2, and applies bias and activation on the accumulators.  The aggregated block
 // never goes back through HBM, and one workgroup's matrix-core phase overlaps the
@@ -25,6 +25,10 @@ namespace {
 
 constexpr int kRows = 64;  // rows per workgroup: two 32-row matrix-core tiles (measured
                            // faster than one: W fragments are fetched once per 64 rows)
+constexpr int kWaves = 8;  // wavefronts per workgroup (measured: 5 % faster than 4, the
+                           // LDS-bound workgroup count then holds more waves per CU)
+constexpr int kThreads = 64 * kWaves;
+constexpr int kColsPerWave = 256 / kWaves;  // output columns a wavefront owns per 256-column chunk
 
 // W (k_in x n, row pitch ldw) -> three bf16 planes [3][n][kp], k-contiguous, zero
 // for k >= k_in.  One thread per (column, pair of k).
@@ -59,7 +63,7 @@ struct FusedArgs {
 
 // KR rows per workgroup (KR / 32 matrix-core tiles along m), four wavefronts.
 template <int LANES, int KR>
-__global__ void __launch_bounds__(256) k_agg_gemm(FusedArgs f) {
+__global__ void __launch_bounds__(kThreads) k_agg_gemm(FusedArgs f) {
   constexpr int TM = KR / 32;
   constexpr int PITCH = LANES * 4 + 8;  // bf16 per plane row (a multiple of 8)
   constexpr int PLANE = KR * PITCH;
@@ -72,8 +76,8 @@ __global__ void __launch_bounds__(256) k_agg_gemm(FusedArgs f) {
   const int64_t r0 = (int64_t)blockIdx.x * KR;
   const bool cok = L.c0 < p.w;
   const bool cfull = L.c0 + 4 <= p.w;
-  const int iters = KR / (4 * groups);
-  auto row_of = [&](int it) { return r0 + (int64_t)(it * 4 + wave) * groups + grp; };
+  const int iters = KR / (kWaves * groups);
+  auto row_of = [&](int it) { return r0 + (int64_t)(it * kWaves + wave) * groups + grp; };
 
   // ---- aggregation.  Two-stage prefetch along the wavefront's rows: the offsets of row
   // it + 2 and the first index chunk of row it + 1 are requested before the gathers of
@@ -159,9 +163,9 @@ __global__ void __launch_bounds__(256) k_agg_gemm(FusedArgs f) {
   const int ksteps = f.kp / 16;
   const int64_t wplane = (int64_t)f.f_out * f.kp;
   const bool full_rows = r0 + KR <= p.n;
-  for (int64_t n0 = (int64_t)wave * 64; n0 < f.f_out; n0 += 256) {
+  for (int64_t n0 = (int64_t)wave * kColsPerWave; n0 < f.f_out; n0 += 256) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < kColsPerWave / 32; ++j) {
       const int64_t col = n0 + j * 32 + l32;
       if (n0 + j * 32 >= f.f_out) break;  // wave-uniform
       // columns past f_out are computed from the last one and never stored
@@ -257,10 +261,10 @@ gcn_status launch_agg_gemm(const AggParams& a, int64_t nnz, const gcn_split* spl
   const dim3 grid((unsigned)ceil_div(a.n, kRows));
   if (a.w <= 64) {
     f.slots = agg_slots(16, nnz, a.n);
-    hipLaunchKernelGGL((k_agg_gemm<16, kRows>), grid, dim3(256), 0, s, f);
+    hipLaunchKernelGGL((k_agg_gemm<16, kRows>), grid, dim3(kThreads), 0, s, f);
   } else {
     f.slots = agg_slots(32, nnz, a.n);
-    hipLaunchKernelGGL((k_agg_gemm<32, kRows>), grid, dim3(256), 0, s, f);
+    hipLaunchKernelGGL((k_agg_gemm<32, kRows>), grid, dim3(kThreads), 0, s, f);
   }
   return check_launch("aggregate-transform");
 }
