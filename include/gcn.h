@@ -419,6 +419,11 @@ int32_t gcn_profile_count(void);
 gcn_status gcn_profile_read(int32_t i, gcn_profile_record* rec);
 /* Drop all records (keeps recording enabled). */
 gcn_status gcn_profile_reset(void);
+/* Record only launches whose family name is exactly `name` (NULL or "": every
+ * launch).  Each event pair costs a few microseconds of queue time between
+ * kernels, so a timed run brackets only the launches it reports.  The name is
+ * copied; at most 63 characters (GCN_E_INVALID beyond). */
+gcn_status gcn_profile_only(const char* name);
 
 #ifdef __cplusplus
 }

@@ -3,6 +3,7 @@
 // When enabled, every aggregation / GEMM launcher records an event pair on its
 // stream around the kernel(s) it enqueues.  Events come from a fixed pool
 // created at enable time; records beyond the capacity overwrite the oldest.
+#include <cstring>
 #include <mutex>
 #include <vector>
 
@@ -20,12 +21,14 @@ std::mutex g_mu;
 std::vector<Record> g_ring;
 int64_t g_next = 0;  // total records started
 bool g_on = false;
+char g_only[64] = "";  // record only this family when non-empty
 
 }  // namespace
 
 ProfScope::ProfScope(const char* name, int32_t width, int64_t rows, int64_t nnz, hipStream_t s) {
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_on || g_ring.empty()) return;
+  if (g_only[0] && strcmp(g_only, name) != 0) return;
   slot = (int)(g_next % (int64_t)g_ring.size());
   ++g_next;
   Record& r = g_ring[slot];
@@ -84,6 +87,13 @@ extern "C" gcn_status gcn_profile_read(int32_t i, gcn_profile_record* rec) {
   GCN_HIP(hipEventElapsedTime(&ms, r.start, r.stop), "profile elapsed");
   r.meta.ms = ms;
   *rec = r.meta;
+  return GCN_OK;
+}
+
+extern "C" gcn_status gcn_profile_only(const char* name) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (name && strlen(name) >= sizeof g_only) return fail(GCN_E_INVALID, "gcn_profile_only: name too long");
+  snprintf(g_only, sizeof g_only, "%s", name ? name : "");
   return GCN_OK;
 }
 

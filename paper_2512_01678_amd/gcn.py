@@ -110,6 +110,7 @@ _SIG = {
     "gcn_profile_count": (i32, []),
     "gcn_profile_read": (i32, [i32, C.POINTER(gcn_profile_record)]),
     "gcn_profile_reset": (i32, []),
+    "gcn_profile_only": (i32, [C.c_char_p]),
 }
 for _name, (_res, _args) in _SIG.items():
     _f = getattr(_lib, _name)
@@ -491,6 +492,11 @@ def profile_records():
 
 def profile_reset():
     _check(_lib.gcn_profile_reset(), "gcn_profile_reset")
+
+
+def profile_only(name=None):
+    """Record only launches of the kernel family `name` (None: every launch)."""
+    _check(_lib.gcn_profile_only(None if name is None else name.encode()), "gcn_profile_only")
 
 
 def raw_lib():

@@ -125,6 +125,10 @@ def test_host_validation_rejects_bad_calls(G):
     # profile read out of range
     rec = G.gcn_profile_record()
     assert L.gcn_profile_read(0, C.byref(rec)) == G.E_INVALID
+    # family filter: name length bound, NULL clears
+    assert L.gcn_profile_only(b"x" * 64) == G.E_INVALID
+    assert L.gcn_profile_only(b"aggregate_w256") == G.OK
+    assert L.gcn_profile_only(None) == G.OK
 
 
 def test_layer_validation(G):
