@@ -104,8 +104,11 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
     }
     float* out = p.Z + row * p.ldz + c0;
     if (VEC == 4 && c0 + 4 <= p.w) {
-      *reinterpret_cast<float4*>(out) = make_float4(z[0], z[VEC > 1 ? 1 : 0], z[VEC > 2 ? 2 : 0],
-                                                    z[VEC > 3 ? 3 : 0]);
+      // written once and not read by this kernel: a non-temporal store leaves L2 to the
+      // gathered rows
+      typedef float f32x4 __attribute__((ext_vector_type(4)));
+      const f32x4 o = {z[0], z[VEC > 1 ? 1 : 0], z[VEC > 2 ? 2 : 0], z[VEC > 3 ? 3 : 0]};
+      __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(out));
     } else {
 #pragma unroll
       for (int i = 0; i < VEC; ++i)

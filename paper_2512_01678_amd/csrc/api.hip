@@ -174,6 +174,11 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     int32_t* id_col = softmax ? a.take<int32_t>(n) : nullptr;
     float* row_loss = softmax ? a.take<float>(n) : nullptr;
     void* cws = softmax ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+    // H_out = P W (+ b) when the fused kernel does not run (split weight in the workspace)
+    GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, softmax ? Zs : Hout,
+                        softmax ? ldz : L->ld_out);
+    q.bias = b;
+    void* gws = a.take<char>((int64_t)gemm_workspace(q));
     if (run && L->agg == GCN_AGG_MAX) {
       AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in);
       int32_t* arg = reinterpret_cast<int32_t*>(saved + (int64_t)n * L->ld_in);
@@ -184,9 +189,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
         AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in, L->agg);
         GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
       }
-      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Zs, ldz);
-      q.bias = b;
-      GCN_TRY(launch_gemm(q, nullptr, s));
+      GCN_TRY(launch_gemm(q, gws, s));
       GCN_TRY(launch_identity_csr(n, id_ptr, id_col, s));
       AggParams z{};
       z.n = n;
@@ -209,11 +212,9 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
       GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
       return GCN_OK;
     }
+    q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
     if (run && L->agg == GCN_AGG_MAX) {
-      GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
-      q.bias = b;
-      q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
-      GCN_TRY(launch_gemm(q, nullptr, s));
+      GCN_TRY(launch_gemm(q, gws, s));
       return GCN_OK;
     }
     if (run) {
@@ -223,10 +224,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
                                 L->ld_out, aws, s));
       } else {
         GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
-        GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, Hout, L->ld_out);
-        q.bias = b;
-        q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
-        GCN_TRY(launch_gemm(q, nullptr, s));
+        GCN_TRY(launch_gemm(q, gws, s));
       }
     }
     return GCN_OK;
@@ -237,6 +235,8 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   float* row_loss = L->act == GCN_ACT_SOFTMAX_CE ? a.take<float>(n) : nullptr;
   void* cws = L->act == GCN_ACT_SOFTMAX_CE ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
   void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_out));
+  const GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
+  void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(q));
   if (!run) return GCN_OK;
   if (x) {
     AggParams p{};
@@ -253,8 +253,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.tag = "spmm_xw";
     GCN_TRY(launch_aggregate(p, x->nnz, nullptr, nullptr, s));
   } else {
-    GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
-    GCN_TRY(launch_gemm(q, nullptr, s));
+    GCN_TRY(launch_gemm(q, gws, s));
   }
   AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out, L->agg);
   p.bias = b;
@@ -287,12 +286,13 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     const int64_t ldt = pitch4(L->f_in);
     float* T = Gprev ? a.take<float>((int64_t)n * ldt) : nullptr;
     void* aws = Gprev ? a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_in)) : nullptr;
+    const GemmParams t = gemm(n, L->f_in, L->f_out, G, L->ld_out, false, W, L->f_out, true, T, ldt);
+    void* tws = Gprev ? a.take<char>((int64_t)gemm_workspace(t)) : nullptr;
     if (!run) return GCN_OK;
     GCN_TRY(launch_gemm(dw, gws, s));
     GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
     if (Gprev) {
-      GemmParams t = gemm(n, L->f_in, L->f_out, G, L->ld_out, false, W, L->f_out, true, T, ldt);
-      GCN_TRY(launch_gemm(t, nullptr, s));
+      GCN_TRY(launch_gemm(t, tws, s));
       AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in, agg_transpose(L->agg));
       if (L->agg == GCN_AGG_MAX) {
         // each (G W^T)[v,c] goes back to the saved maximiser of (v, c)
@@ -315,6 +315,11 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   const size_t agg_need = std::max(aggregate_workspace(&g->split, L->f_out),
                                    x && x->col_ptr ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
   void* aws = a.take<char>((int64_t)agg_need);
+  GemmParams t = gemm(n, L->f_in, L->f_out, Q, ldq, false, W, L->f_out, true, Gprev, L->ld_in);
+  t.epi = GEMM_MASK;
+  t.mask = Hin;
+  t.ldmask = L->ld_in;
+  void* tws = Gprev ? a.take<char>((int64_t)gemm_workspace(t)) : nullptr;
   if (!run) return GCN_OK;
   GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq, agg_transpose(L->agg)), g->nnz,
                            &g->split, aws, s));
@@ -339,13 +344,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     GCN_TRY(launch_gemm(dw, gws, s));
   }
   GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
-  if (Gprev) {
-    GemmParams t = gemm(n, L->f_in, L->f_out, Q, ldq, false, W, L->f_out, true, Gprev, L->ld_in);
-    t.epi = GEMM_MASK;
-    t.mask = Hin;
-    t.ldmask = L->ld_in;
-    GCN_TRY(launch_gemm(t, nullptr, s));
-  }
+  if (Gprev) GCN_TRY(launch_gemm(t, tws, s));
   return GCN_OK;
 }
 
@@ -630,7 +629,7 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
   GCN_TRY(ws_protocol(d_ws, ws_bytes, gemm_workspace(p), "gcn_gemm", &query));
   if (query) return GCN_OK;
   if (m > 0 && n > 0 && (!d_C || (k > 0 && (!d_A || !d_B)))) return fail(GCN_E_INVALID, "gcn_gemm: NULL operand");
-  if (gemm_workspace(p) > 0 && p.epi != GEMM_NONE)
+  if (gemm_split_k(p) && p.epi != GEMM_NONE)
     return fail(GCN_E_UNSUPPORTED, "gcn_gemm: split-k launches support only the bias epilogue");
   return launch_gemm(p, d_ws, stream);
 }

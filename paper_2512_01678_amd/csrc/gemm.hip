@@ -39,6 +39,7 @@ namespace {
 
 
 constexpr int kPad = 4;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 
 struct GemmArgs {
@@ -365,7 +366,9 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   // Epilogue, one wave-row of the tile (RB rows) per round: the waves of that row
   // put their accumulators in LDS (lane l32 holds column l32 of a 32x32 sub-tile,
   // register r row 8*(r/4) + 4*h + r%4), then the whole workgroup streams the RB x BN
-  // slab out as row-contiguous 16-byte accesses (mask, bias, C or the split-k partial).
+  // slab out as row-contiguous 16-byte accesses (mask, bias, C or the split-k partial);
+  // the mask and C streams are touched once (non-temporal, leaving L2 to the operands).
+  // Split-k partials are stored normally: the reduce reads them back at once.
   float* const tile = smem;
   const int64_t ldo = SPLIT ? p.n : p.ldc;
   float* const out = SPLIT ? g.part + (int64_t)blockIdx.z * p.m * p.n : p.C;
@@ -398,8 +401,8 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
         if (EPI == GEMM_MASK) {
           const float* mp = p.mask + row * p.ldmask + col;
           if (mvec && full) {
-            const float4 m4 = *reinterpret_cast<const float4*>(mp);
-            mk[0] = m4.x; mk[1] = m4.y; mk[2] = m4.z; mk[3] = m4.w;
+            const f32x4 m4 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mp));
+            mk[0] = m4[0]; mk[1] = m4[1]; mk[2] = m4[2]; mk[3] = m4[3];
           } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q) mk[q] = col + q < p.n ? mp[q] : 0.f;
@@ -414,7 +417,9 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
       }
       float* op = out + row * ldo + col;
       if (ovec && full) {
-        *reinterpret_cast<float4*>(op) = make_float4(v[0], v[1], v[2], v[3]);
+        const f32x4 o = {v[0], v[1], v[2], v[3]};
+        if (SPLIT) *reinterpret_cast<f32x4*>(op) = o;  // partials: read back at once by the reduce
+        else __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(op));
       } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
@@ -534,7 +539,12 @@ bool gemm_bf16x6_mode() {
   return !(e && strcmp(e, "fp32") == 0);
 }
 
+bool gemm_split_k(const GemmParams& p) {
+  return !gemm_rows_supported(p) && p.k > 0 && pick_splits(p, pick_shape(p, use_emulation(p))) > 1;
+}
+
 size_t gemm_workspace(const GemmParams& p) {
+  if (gemm_rows_supported(p)) return gemm_rows_workspace(p);
   const Shape sh = pick_shape(p, use_emulation(p));
   const int64_t s = pick_splits(p, sh);
   return s > 1 ? sizeof(float) * (size_t)(s * p.m * p.n) : 0;
@@ -542,6 +552,13 @@ size_t gemm_workspace(const GemmParams& p) {
 
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   if (p.m == 0 || p.n == 0) return GCN_OK;
+  if (gemm_rows_supported(p)) {
+    if (!ws) return fail(GCN_E_INVALID, "gemm: the row-panel product needs its workspace");
+    char name[64];
+    snprintf(name, sizeof name, "gemm_%s_%ldx%ldx%ld", p.tb ? "NT" : "NN", (long)p.m, (long)p.n, (long)p.k);
+    ProfScope prof(name, (int32_t)p.n, p.m, p.k, s);
+    return launch_gemm_rows(p, ws, s);
+  }
   const bool emu = use_emulation(p);
   const Shape sh = pick_shape(p, emu);
   const int64_t splits = p.k == 0 ? 1 : pick_splits(p, sh);

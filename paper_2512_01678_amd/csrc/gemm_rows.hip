@@ -1,0 +1,336 @@
+// gemm_rows.hip -- C = A B for a tall A and a small B (n <= 256), bf16x6 arithmetic.
+//
+// The transform products of a GCN layer multiply an N x k feature matrix by a k x n
+// weight (H W forward, Q W^T for the input gradient, Section II-A / Algorithm 1), with N
+// in the hundreds of thousands and k, n at most a few hundred.  The general tiled GEMM
+// re-splits the weight in every workgroup and reads each row of A once per 128 output
+// columns; here instead:
+//  * B is split once per call (k_split_b) into three bf16 planes stored in the exact
+//    order the matrix-core fragments consume them: block (slab, step, column tile,
+//    plane) holds, for lane l, the 8 bf16 of column 32 j + l % 32 at the 8 k positions
+//    that lane feeds to v_mfma_f32_32x32x16_bf16 (1 KB per block, one 16-byte read per
+//    lane, no bank conflicts);
+//  * a wavefront owns 32 rows of C and every output column, so each element of A is
+//    loaded from HBM and split exactly once.  A goes straight from global memory into
+//    the fragment registers (no LDS, no barrier): within a 32-wide k slab, lane half h
+//    of row r loads k = 8 i + 4 h .. + 3 for i = 0..3 (32 contiguous bytes per row and
+//    load), and MFMA step t takes the loads i = 2t, 2t+1 -- a fixed permutation of k
+//    inside the slab, applied identically to B by the split, which a sum over k does
+//    not see;
+//  * the four wavefronts of a workgroup (128 rows) share B through LDS one 16-k step at
+//    a time, double-buffered: the next step is read from L2 while the current one
+//    feeds the matrix cores, with one barrier per step; two workgroups share a CU;
+//  * the epilogue (bias, ReLU) stages the accumulators through LDS and writes C in
+//    256-byte row segments with non-temporal stores.
+// Products with the 1[mask > 0] epilogue use the tiled kernel of gemm.hip.
+// The arithmetic per product is that of gemm.hip's bf16x6 mode (the same six part
+// products, fp32 accumulation), summed in a different order.
+#include <cstdlib>
+#include <cstring>
+
+#include "bf16x6.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kRowsPerWave = 32;
+constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
+constexpr int kSlab = 32;          // k per slab: two 32x32x16 steps
+constexpr int kBlockBf16 = 64 * 8;  // one fragment block: 64 lanes x 8 bf16 (1 KB)
+constexpr int kStagePitch = 64 + 4;   // floats per staged epilogue row
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Slab-local k of MFMA step t, lane half h, fragment element e (0..7).
+__host__ __device__ constexpr int kmap(int t, int h, int e) { return 16 * t + 8 * (e >> 2) + 4 * h + (e & 3); }
+
+struct RowsArgs {
+  GemmParams p;
+  const __bf16* bp;  // split B: [slab][step][column tile][plane][lane][8]
+  int nj;            // column tiles (ceil(n / 32))
+  int64_t nslab;
+  int c_vec;         // C rows 16-byte aligned with ldc % 4 == 0
+};
+
+// One thread per (slab, step, column tile, lane): 8 values of B, split into 3 planes.
+__global__ void __launch_bounds__(256) k_split_b(RowsArgs r, int64_t total, __bf16* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  const GemmParams& p = r.p;
+  const int l = (int)(i % 64);
+  const int64_t blk = i / 64;  // (slab * 2 + t) * nj + j
+  const int j = (int)(blk % r.nj);
+  const int64_t st = blk / r.nj;
+  const int t = (int)(st % 2);
+  const int64_t s = st / 2;
+  const int64_t col = (int64_t)j * 32 + l % 32;
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int64_t k = s * kSlab + kmap(t, l / 32, e);
+    v[e] = 0.f;
+    if (k < p.k && col < p.n) v[e] = p.tb ? p.B[col * p.ldb + k] : p.B[k * p.ldb + col];
+  }
+  uint4 hi, mid, lo;
+  split_pair(v[0], v[1], hi.x, mid.x, lo.x);
+  split_pair(v[2], v[3], hi.y, mid.y, lo.y);
+  split_pair(v[4], v[5], hi.z, mid.z, lo.z);
+  split_pair(v[6], v[7], hi.w, mid.w, lo.w);
+  uint4* o = reinterpret_cast<uint4*>(out + (blk * 3) * kBlockBf16) + l;
+  o[0] = hi;
+  o[64] = mid;
+  o[128] = lo;
+}
+
+// Split 8 fp32 (two float4) into the three bf16x8 fragment parts.
+__device__ __forceinline__ void split8(const float4& a, const float4& b, bf16x8& hi, bf16x8& mid, bf16x8& lo) {
+  uint4 h, m, o;
+  split_pair(a.x, a.y, h.x, m.x, o.x);
+  split_pair(a.z, a.w, h.y, m.y, o.y);
+  split_pair(b.x, b.y, h.z, m.z, o.z);
+  split_pair(b.z, b.w, h.w, m.w, o.w);
+  hi = __builtin_bit_cast(bf16x8, h);
+  mid = __builtin_bit_cast(bf16x8, m);
+  lo = __builtin_bit_cast(bf16x8, o);
+}
+
+// NJ column tiles of 32; PD slabs of A in flight per wavefront.
+// Two wavefronts per SIMD (two workgroups per CU): one workgroup's epilogue and barrier
+// waits overlap the other's matrix work.
+template <int NJ, int PD, int EPI>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) k_gemm_rows(RowsArgs r) {
+  constexpr int kStepBf16 = NJ * 3 * kBlockBf16;  // B of one 16-k step
+  constexpr int kChunks = kStepBf16 / 8;          // 16-byte pieces per step
+  constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
+  // two B steps during the k walk, then the epilogue staging (32 x 68 floats per wave)
+  constexpr int kStageBf16 = 2 * kWaves * kRowsPerWave * kStagePitch;
+  constexpr int kLdsBf16 = 2 * kStepBf16 > kStageBf16 ? 2 * kStepBf16 : kStageBf16;
+  __shared__ __attribute__((aligned(16))) __bf16 lds[kLdsBf16];
+
+  const GemmParams& p = r.p;
+  const int tid = threadIdx.x, l = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // wave-uniform: scalar registers
+  const int h = l / 32, l32 = l % 32;
+  const int64_t row0 = (int64_t)blockIdx.x * kRowsPerBlock + (int64_t)wave * kRowsPerWave;
+  const int64_t nslab = r.nslab, nstep = 2 * nslab;
+
+  // this lane's A row (rows past the end re-read the last row; never stored)
+  const int64_t arow = row0 + l32 < p.m ? row0 + l32 : p.m - 1;
+  const float* ap = p.A + arow * p.lda + 4 * h;
+  const bool kfull = p.k % kSlab == 0;
+  auto load_a = [&](int64_t s, float4 (&ra)[4]) __attribute__((always_inline)) {
+    const float* q = ap + s * kSlab;
+    if (kfull || (s + 1) * kSlab <= p.k) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ra[i] = *reinterpret_cast<const float4*>(q + 8 * i);
+    } else {
+      // partial last slab: zeros past k (the split B is zero there too)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t k0 = s * kSlab + 8 * i + 4 * h;
+        float t4[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) t4[c] = k0 + c < p.k ? q[8 * i + c] : 0.f;
+        ra[i] = make_float4(t4[0], t4[1], t4[2], t4[3]);
+      }
+    }
+  };
+  const u32x4* bsrc = reinterpret_cast<const u32x4*>(r.bp);
+  auto load_b = [&](int64_t g, u32x4 (&rb)[kPer]) __attribute__((always_inline)) {
+    const u32x4* q = bsrc + g * kChunks;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      if (kChunks % kThreads == 0 || tid + i * kThreads < kChunks) rb[i] = q[tid + i * kThreads];
+  };
+  auto store_b = [&](int buf, const u32x4 (&rb)[kPer]) __attribute__((always_inline)) {
+    u32x4* q = reinterpret_cast<u32x4*>(lds + buf * kStepBf16);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      if (kChunks % kThreads == 0 || tid + i * kThreads < kChunks) q[tid + i * kThreads] = rb[i];
+  };
+
+  floatx16 acc[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+
+  static_assert(PD >= 1 && PD <= 3, "A slabs in flight: 1 to 3");
+  float4 ra[PD][4];
+  u32x4 rb[kPer];
+  load_a(0, ra[0]);  // nslab >= 1 (k > 0)
+  if constexpr (PD > 1)
+    if (nslab > 1) load_a(1, ra[1]);
+  if constexpr (PD > 2)
+    if (nslab > 2) load_a(2, ra[2]);
+  load_b(0, rb);
+  store_b(0, rb);
+  __syncthreads();
+
+  // one MFMA step (16 k) of every column tile with the A parts of this lane's row; two
+  // tiles at a time, their accumulation chains interleaved
+  auto step = [&](int buf, const bf16x8& ah, const bf16x8& am, const bf16x8& al) __attribute__((always_inline)) {
+    const bf16x8* f0 = reinterpret_cast<const bf16x8*>(lds + buf * kStepBf16) + l;
+#pragma unroll
+    for (int j = 0; j + 1 < NJ; j += 2) {
+      const bf16x8* f = f0 + j * 3 * 64;
+      const bf16x8 bh0 = f[0], bm0 = f[64], bo0 = f[128], bh1 = f[192], bm1 = f[256], bo1 = f[320];
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh1, acc[j + 1], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bm0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bm1, acc[j + 1], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bo0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bo1, acc[j + 1], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bh0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bh1, acc[j + 1], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bm0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bm1, acc[j + 1], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh0, acc[j], 0, 0, 0);
+      acc[j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh1, acc[j + 1], 0, 0, 0);
+    }
+    if constexpr (NJ % 2 == 1) {
+      const bf16x8* f = f0 + (NJ - 1) * 3 * 64;
+      const bf16x8 bh = f[0], bm = f[64], bo = f[128];
+      floatx16& c = acc[NJ - 1];
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bm, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bo, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am, bh, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bm, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, c, 0, 0, 0);
+    }
+  };
+  // slab s (steps 2s in LDS buffer 0 and 2s + 1 in buffer 1), whose A values are in cur
+  // (refilled with slab s + PD).  The B of the next step is read from L2 while the
+  // current step runs; a buffer is rewritten only after the barrier that ends the step
+  // which last read it.
+  auto slab = [&](int64_t s, float4 (&cur)[4]) __attribute__((always_inline)) {
+    if (s >= nslab) return;
+    const int64_t g = 2 * s;
+    load_b(g + 1, rb);
+    bf16x8 ah0, am0, al0, ah1, am1, al1;
+    split8(cur[0], cur[1], ah0, am0, al0);
+    split8(cur[2], cur[3], ah1, am1, al1);
+    if (s + PD < nslab) load_a(s + PD, cur);
+    step(0, ah0, am0, al0);
+    store_b(1, rb);
+    __syncthreads();
+    if (g + 2 < nstep) load_b(g + 2, rb);
+    step(1, ah1, am1, al1);
+    if (g + 2 < nstep) store_b(0, rb);
+    __syncthreads();
+  };
+  for (int64_t s0 = 0; s0 < nslab; s0 += PD) {
+    slab(s0, ra[0]);
+    if constexpr (PD > 1) slab(s0 + 1, ra[1]);
+    if constexpr (PD > 2) slab(s0 + 2, ra[2]);
+  }
+
+  // Epilogue, two column tiles (32 rows x 64 columns) at a time per wavefront: the
+  // accumulators (lane l32 holds column l32 of rows 8 (e / 4) + 4 h + e % 4) go to this
+  // wavefront's part of the LDS, which the B steps no longer use (the last step ended
+  // with a barrier), and come back as row-contiguous 16-byte vectors, so that C is written
+  // in 256-byte row segments (bias and ReLU apply there).  C is touched once: non-temporal
+  // stores keep it from displacing the split B in L2 (measured: 20 % faster on the
+  // 169,343 x 256 x 256 product).
+  float* stage = reinterpret_cast<float*>(lds) + wave * kRowsPerWave * kStagePitch;
+  const int sr = l / 16, sc = 4 * (l % 16);  // read-back: rows sr + 4 i, columns sc .. sc + 3
+#pragma unroll
+  for (int j0 = 0; j0 < NJ; j0 += 2) {
+#pragma unroll
+    for (int jj = 0; jj < 2 && j0 + jj < NJ; ++jj)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) stage[(8 * (e / 4) + 4 * h + e % 4) * kStagePitch + 32 * jj + l32] = acc[j0 + jj][e];
+    // the wavefront's own staging area: LDS accesses of one wavefront complete in order,
+    // the fence keeps the compiler from reordering them
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int64_t col = (int64_t)j0 * 32 + sc;
+    if (col < p.n) {
+      const bool full = col + 4 <= p.n;
+      float bias[4] = {0.f, 0.f, 0.f, 0.f};
+      if (p.bias)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bias[q] = col + q < p.n ? p.bias[col + q] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int64_t row = row0 + sr + 4 * i;
+        if (row >= p.m) continue;
+        const float4 t = *reinterpret_cast<const float4*>(stage + (sr + 4 * i) * kStagePitch + sc);
+        float v[4] = {t.x + bias[0], t.y + bias[1], t.z + bias[2], t.w + bias[3]};
+        if constexpr (EPI == GEMM_RELU)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.f);
+        float* cp = p.C + row * p.ldc + col;
+        if (full && r.c_vec) {
+          const f32x4 o = {v[0], v[1], v[2], v[3]};
+          __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(cp));
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (col + q < p.n) cp[q] = v[q];
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // before the next pair's writes
+  }
+}
+
+template <int NJ, int PD>
+void launch_nj(const RowsArgs& r, hipStream_t s) {
+  const dim3 grid((unsigned)ceil_div(r.p.m, kRowsPerBlock));
+  switch (r.p.epi) {
+    case GEMM_RELU: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_RELU>), grid, dim3(kThreads), 0, s, r); break;
+    default: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_NONE>), grid, dim3(kThreads), 0, s, r);
+  }
+}
+
+int64_t split_b_elems(const GemmParams& p) {
+  return ceil_div(p.k, kSlab) * 2 * ceil_div(p.n, 32) * 3 * kBlockBf16;
+}
+
+}  // namespace
+
+// GCN_GEMM_ROWS=0 sends these products to the general tiled kernel (for comparison).
+static bool rows_enabled() {
+  const char* e = getenv("GCN_GEMM_ROWS");
+  return !(e && strcmp(e, "0") == 0);
+}
+
+// Products with the mask epilogue (the input gradient) stay on the tiled kernel, measured
+// faster there on the arxiv-like shapes.
+bool gemm_rows_supported(const GemmParams& p) {
+  return gemm_bf16x6_mode() && rows_enabled() && p.epi != GEMM_MASK && !p.ta && p.n > 0 && p.n <= 256 && p.k > 0 && p.m >= kRowsPerBlock &&
+         p.lda % 4 == 0 && aligned16(p.A);
+}
+
+size_t gemm_rows_workspace(const GemmParams& p) {
+  return gemm_rows_supported(p) ? sizeof(__bf16) * (size_t)split_b_elems(p) : 0;
+}
+
+gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
+  RowsArgs r{};
+  r.p = p;
+  r.nj = (int)ceil_div(p.n, 32);
+  r.nslab = ceil_div(p.k, kSlab);
+  r.bp = static_cast<const __bf16*>(ws);
+  r.c_vec = p.ldc % 4 == 0 && aligned16(p.C);
+  const int64_t threads = r.nslab * 2 * r.nj * 64;
+  hipLaunchKernelGGL(k_split_b, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, s, r, threads,
+                     static_cast<__bf16*>(ws));
+  GCN_TRY(check_launch("gemm weight split"));
+  switch (r.nj) {
+    case 1: launch_nj<1, 3>(r, s); break;
+    case 2: launch_nj<2, 3>(r, s); break;
+    case 3: launch_nj<3, 2>(r, s); break;
+    case 4: launch_nj<4, 2>(r, s); break;
+    case 5: launch_nj<5, 2>(r, s); break;
+    case 6: launch_nj<6, 1>(r, s); break;
+    case 7: launch_nj<7, 1>(r, s); break;
+    default: launch_nj<8, 1>(r, s);
+  }
+  return check_launch("gemm (row panels)");
+}
+
+}  // namespace gcn

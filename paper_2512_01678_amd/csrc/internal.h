@@ -153,7 +153,13 @@ struct GemmParams {
   const float* mask;
   int64_t ldmask;
 };
+// Workspace of launch_gemm: split-k partials (A^T B), or the split B of the row-panel
+// product (A B, A B^T with n <= 256); 0 when neither applies.
 size_t gemm_workspace(const GemmParams& p);
+bool gemm_split_k(const GemmParams& p);
+bool gemm_rows_supported(const GemmParams& p);
+size_t gemm_rows_workspace(const GemmParams& p);
+gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s);
 // Arithmetic of the dense products: bf16x6 (default) unless GCN_GEMM_MODE=fp32.
 bool gemm_bf16x6_mode();
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s);
