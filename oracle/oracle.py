@@ -336,7 +336,8 @@ def forward_aux(g: Graph, X, Ws, bs, sparse: SparseX | None = None, aggs=None):
     return Hs, Zs, aux
 
 
-def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=None, aux=None):
+def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=None, aux=None,
+             relu_on=None):
     """Gradients of the mean loss for every layer (Algorithm 1, Backward).
 
     Linear layers: Q_l = S_l^T G_l (A_hat and A + I are symmetric, the mean's transpose
@@ -344,9 +345,15 @@ def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=N
     G_{l-1} = (Q_l W_l^T) * 1[Z_{l-1} > 0].
     Max layers: dW_l = P_l^T G_l;  G_{l-1} = maxgrad(G_l W_l^T) * 1[Z_{l-1} > 0].
     db_l = sum_i G_l[i,:].  Returns (dWs, dbs, Gs) with Gs[l] = dLoss/dZ_l.
+
+    relu_on: optional list; relu_on[l] (boolean, the shape of Z_l) replaces 1[Z_l > 0],
+    so that a comparison can take the ReLU decisions where another implementation took
+    them (a decision on a pre-activation within rounding of zero is precision-dependent).
     """
     L = len(Ws)
     aggs = aggs or ["gcn"] * L
+    on = [relu_on[l] if relu_on is not None and relu_on[l] is not None else (Zs[l] > 0.0)
+          for l in range(L - 1)]
     dWs, dbs, Gs = [None] * L, [None] * L, [None] * L
     G = np.asarray(G_last, np.float64)
     for l in range(L - 1, -1, -1):
@@ -357,7 +364,7 @@ def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=N
             P, arg = aux[l]
             dWs[l] = matmul(P.T, G)
             if l > 0:
-                G = aggregate_max_backward(g, matmul(G, Wt), arg) * (Zs[l - 1] > 0.0)
+                G = aggregate_max_backward(g, matmul(G, Wt), arg) * on[l - 1]
             continue
         Q = aggregate(g, G, kind=TRANSPOSE[aggs[l]])
         if l == 0 and sparse is not None:
@@ -366,20 +373,23 @@ def backward(g: Graph, Hs, Zs, G_last, Ws, sparse: SparseX | None = None, aggs=N
         else:
             dWs[l] = matmul(Hs[l].T, Q)
         if l > 0:
-            G = matmul(Q, Wt) * (Zs[l - 1] > 0.0)
+            G = matmul(Q, Wt) * on[l - 1]
     return dWs, dbs, Gs
 
 
 def epoch(g: Graph, X, y, Ws, bs, mW, vW, mb, vb, t: int, sparse: SparseX | None = None,
-          lr=0.01, b1=0.9, b2=0.999, eps=1e-8, aggs=None):
+          lr=0.01, b1=0.9, b2=0.999, eps=1e-8, aggs=None, relu_on=None):
     """One training epoch: forward, softmax-CE loss, backward, Adam step t (t >= 1).
 
-    aggs: per-layer aggregator ("gcn" default, "sum", "mean", "max").
-    Returns a dict with loss, activations, gradients and updated parameters/state.
+    aggs: per-layer aggregator ("gcn" default, "sum", "mean", "max").  relu_on: optional
+    callable (Zs -> list of boolean masks) giving the backward's ReLU decisions (see
+    backward).  Returns a dict with loss, activations, gradients and updated
+    parameters/state.
     """
     Hs, Zs, aux = forward_aux(g, X, Ws, bs, sparse, aggs)
     loss, G, _ = softmax_ce(Zs[-1], y)
-    dWs, dbs, Gs = backward(g, Hs, Zs, G, Ws, sparse, aggs, aux)
+    dWs, dbs, Gs = backward(g, Hs, Zs, G, Ws, sparse, aggs, aux,
+                            relu_on=relu_on(Zs) if relu_on is not None else None)
     nW, nmW, nvW, nb, nmb, nvb = [], [], [], [], [], []
     for l in range(len(Ws)):
         a, m_, v_ = adam(Ws[l], dWs[l], mW[l], vW[l], t, lr, b1, b2, eps)

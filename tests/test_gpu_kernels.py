@@ -469,9 +469,12 @@ def test_softmax_layer_on_split_hubs(G, orc, hub_graph):
     np.testing.assert_allclose(host(out), Gr, rtol=0, atol=1e-4 * np.abs(Gr).max())
 
 
+@pytest.mark.parametrize("fused", ["1", "0"])
 @pytest.mark.parametrize("fi,fo", [(128, 256), (48, 300)])
-def test_aggregate_first_layer_on_split_hubs(G, orc, hub_graph, fi, fo):
-    """Fused aggregate-then-transform layer: hub rows come from the chunk kernels."""
+def test_aggregate_first_layer_on_split_hubs(G, orc, hub_graph, fi, fo, fused, monkeypatch):
+    """Aggregate-then-transform layer, fused kernel and two-launch form: hub rows come from
+    the chunk kernels."""
+    monkeypatch.setenv("GCN_AF_FUSED", fused)
     og, dg = hub_graph
     n = og.n
     rng = np.random.default_rng(fi)

@@ -195,6 +195,26 @@ def snapshot(m):
 AGGS = {"gcn": 0, "sum": 1, "mean": 2, "max": 4}
 
 
+def gpu_relu_decisions(m, tag):
+    """The ReLU factor 1[Z_l > 0] of the backward is a decision taken on the fp32
+    pre-activation on the GPU and on the fp64 one in the oracle; where Z_l is within
+    rounding of zero both are correct, and one flipped entry moves G, dW and db of every
+    earlier layer far beyond the comparison tolerance.  The oracle takes the GPU's
+    decisions (1[H_{l+1} > 0]), after checking that they agree with its own everywhere
+    outside a band of 1e-5 max|Z_l| around zero."""
+    def decide(Zs):
+        on = []
+        for l in range(m.L - 1):
+            Z = Zs[l]
+            gpu_on = host(m.act[l])[:, :Z.shape[1]] > 0
+            differ = gpu_on != (Z > 0)
+            band = 1e-5 * np.abs(Z).max()
+            assert not (differ & (np.abs(Z) > band)).any(), f"{tag}: ReLU decided differently away from zero"
+            on.append(gpu_on)
+        return on
+    return decide
+
+
 def run_epochs(G, orc, p, epochs, sparse, aggs=None, csc=True):
     """Each epoch: the oracle starts from the GPU's own pre-epoch parameters and Adam
     state, so every epoch is a well-conditioned comparison (Adam's first steps move
@@ -213,9 +233,9 @@ def run_epochs(G, orc, p, epochs, sparse, aggs=None, csc=True):
     for t in range(1, epochs + 1):
         st = snapshot(m)
         m.epoch(p.dg, X=None if sparse else Xd, x=sx, labels=yd)
-        out = orc.epoch(p.og, p.X, p.y, st["W"], st["b"], st["mW"], st["vW"], st["mb"], st["vb"], t,
-                        sparse=osx, aggs=list(aggs) if aggs else None)
         tag = f"{p.wl.name} epoch {t}"
+        out = orc.epoch(p.og, p.X, p.y, st["W"], st["b"], st["mW"], st["vW"], st["mb"], st["vb"], t,
+                        sparse=osx, aggs=list(aggs) if aggs else None, relu_on=gpu_relu_decisions(m, tag))
         assert host(m.loss)[0] == pytest.approx(out["loss"], rel=1e-4), tag
         for l in range(m.L):
             assert_norm_close(host(m.grad[l]), out["Gs"][l], f"{tag} G_{l}")

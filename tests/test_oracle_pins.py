@@ -477,6 +477,27 @@ def test_epochs_match_torch_training(orc):
         np.testing.assert_allclose(st["bs"][l], bt[l].detach().numpy(), atol=1e-12)
 
 
+def test_backward_relu_decisions_hook(orc):
+    """The optional ReLU decisions of the backward: the oracle's own decisions reproduce
+    the default exactly, and flipping one decision changes only that entry of G (the
+    flipped factor times (Q W^T) there) before it propagates."""
+    src, dst, X, Ws, bs, y = tiny_problem(33, n=25, widths=(5, 6, 3))
+    g = orc.build_csr(25, src, dst)
+    Hs, Zs = orc.forward(g, X, Ws, bs)
+    _, G, _ = orc.softmax_ce(Zs[-1], y)
+    ref = orc.backward(g, Hs, Zs, G, Ws)
+    same = orc.backward(g, Hs, Zs, G, Ws, relu_on=[Zs[0] > 0])
+    for a, b in zip(ref[0] + ref[1] + ref[2], same[0] + same[1] + same[2]):
+        np.testing.assert_array_equal(a, b)
+    on = Zs[0] > 0
+    i, j = np.argwhere(on)[0]
+    on[i, j] = False
+    flip = orc.backward(g, Hs, Zs, G, Ws, relu_on=[on])
+    diff = flip[2][0] != ref[2][0]
+    assert diff.sum() == 1 and diff[i, j] and flip[2][0][i, j] == 0.0
+    np.testing.assert_array_equal(flip[2][1], ref[2][1])  # the last layer's G is upstream
+
+
 # ---------------------------------------------------------------------------
 # other aggregators: sum (A + I), mean (D^-1 (A + I)) and its transpose, max
 # ---------------------------------------------------------------------------
