@@ -35,13 +35,16 @@ namespace {
 
 constexpr int kBlock = 256;
 
-// Bias and epilogue of one row; slice 0 writes.
-template <int LANES, int VEC, int EPI>
+// Bias and epilogue of one row.  Every slice of the group holds the row's total and
+// slice 0 writes; with OWN, each slice holds a row of its own (own: that row exists and
+// is finished here) and writes it.
+template <int LANES, int VEC, int EPI, bool OWN = false>
 __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, const typename Vec<VEC>::T& acc,
-                                           const Lanes& L, bool cok) {
+                                           const Lanes& L, bool cok, bool own = true) {
   using V = Vec<VEC>;
   const int c0 = L.c0;
-  const float sc = row_scale(p, row);
+  const bool writer = OWN ? own : L.slot == 0;
+  const float sc = own ? row_scale(p, row) : 1.f;
   float z[VEC];
 #pragma unroll
   for (int i = 0; i < VEC; ++i) {
@@ -64,13 +67,13 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
       se += e[i];
     }
     se = group_sum<LANES>(se);
-    const int y = p.labels[row];
+    const int y = own ? p.labels[row] : -1;
     float zy = 0.f;
 #pragma unroll
     for (int i = 0; i < VEC; ++i)
       if (c0 + i == y) zy = z[i];
     zy = group_sum<LANES>(zy);
-    if (L.slot != 0) return;
+    if (!writer) return;
     if (L.lane == 0) p.row_loss[row] = (logf(se) + mx) - zy;
     if (!cok) return;
     const float inv_se = 1.f / se;
@@ -93,7 +96,7 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
         if (c0 + i < p.w) lg[i] = z[i];
     }
   } else {
-    if (!cok || L.slot != 0) return;
+    if (!cok || !writer) return;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
       if constexpr (EPI == AGG_RELU) z[i] = fmaxf(z[i], 0.f);
@@ -123,13 +126,35 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
 template <int LANES, int VEC, int EPI>
 __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, int64_t skip_over) {
   const Lanes L = lanes_of<LANES, VEC>(slots);
-  const int64_t row = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
-  if (row >= p.n) return;  // whole groups leave together
-  const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
-  if (end - beg > skip_over) return;
   const bool cok = L.c0 < p.w;
-  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
-  finish_row<LANES, VEC, EPI>(p, row, acc, L, cok);
+  const int64_t g = (int64_t)blockIdx.x * (kBlock / L.gw) + threadIdx.x / L.gw;
+  if constexpr (EPI == AGG_SOFTMAX) {
+    // The loss epilogue (row maximum, exponentials, three slice reductions, the loss and
+    // the gradient row) would cost every slice of a group the same instructions for one
+    // row.  Instead a group sums `slots` consecutive rows one after the other, slice s
+    // keeping row s's total, and then every slice finishes its own row.
+    const int64_t row0 = g * slots;
+    if (row0 >= p.n) return;  // whole groups leave together
+    typename Vec<VEC>::T mine = Vec<VEC>::zero();
+    bool own = false;
+    for (int r = 0; r < slots && row0 + r < p.n; ++r) {
+      const int64_t beg = p.row_ptr[row0 + r], end = p.row_ptr[row0 + r + 1];
+      if (end - beg > skip_over) continue;  // a long row: k_combine finishes it
+      const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
+      if (L.slot == r) {
+        mine = acc;
+        own = true;
+      }
+    }
+    finish_row<LANES, VEC, EPI, true>(p, row0 + L.slot, mine, L, cok, own);
+  } else {
+    const int64_t row = g;
+    if (row >= p.n) return;  // whole groups leave together
+    const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
+    if (end - beg > skip_over) return;
+    const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
+    finish_row<LANES, VEC, EPI>(p, row, acc, L, cok);
+  }
 }
 
 // One group per chunk of a long row: partial[ch, :] = sum over the chunk's entries.
@@ -181,7 +206,8 @@ gcn_status launch3(const Launch& a) {
   const unsigned gy = (unsigned)ceil_div(p.w, LANES * VEC);
   {
     const int gw = LANES * a.slots;
-    dim3 grid((unsigned)ceil_div(p.n, kBlock / gw), gy);
+    const int64_t groups = EPI == AGG_SOFTMAX ? ceil_div(p.n, a.slots) : p.n;  // rows per group
+    dim3 grid((unsigned)ceil_div(groups, kBlock / gw), gy);
     hipLaunchKernelGGL((k_aggregate<LANES, VEC, EPI>), grid, dim3(kBlock), 0, a.s, p, a.slots, skip);
     GCN_TRY(check_launch("aggregate"));
   }
