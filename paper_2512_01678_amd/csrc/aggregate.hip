@@ -96,6 +96,19 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
         if (c0 + i < p.w) lg[i] = z[i];
     }
   } else {
+    if constexpr (EPI == AGG_RELU) {
+      if (p.relu_bits) {
+        // 1[z > 0] of this lane's columns, OR-ed over the lanes of one 32-column word
+        // (every lane of the group takes part before any leaves)
+        constexpr int kWordLanes = LANES < 32 / VEC ? LANES : 32 / VEC;
+        uint32_t bits = 0;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i)
+          if (c0 + i < p.w && z[i] > 0.f) bits |= 1u << ((c0 + i) % 32);
+        bits = group_or<kWordLanes>(bits);
+        if (writer && c0 < p.w && L.lane % kWordLanes == 0) p.relu_bits[row * p.ld_relu_bits + c0 / 32] = bits;
+      }
+    }
     if (!cok || !writer) return;
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {

@@ -154,12 +154,18 @@ GemmParams gemm(int64_t m, int64_t n, int64_t k, const float* A, int64_t lda, bo
 // layer plans: the same function sizes the workspace (base == NULL) and runs
 // ---------------------------------------------------------------------------
 
+// relu_bits (optional, ReLU layers): also write the bitmask 1[H_out > 0] (relu_bits_words
+// words per row) where the producing kernel can; *bits_written tells whether it does (set
+// in the sizing pass too).
 gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, const gcn_sparse_x* x,
                      const float* W, const float* b, float* Hout, float* saved, const int32_t* labels,
-                     float* loss, float* logits, Arena& a, hipStream_t s) {
+                     float* loss, float* logits, Arena& a, hipStream_t s, uint32_t* relu_bits = nullptr,
+                     bool* bits_written = nullptr) {
   const int32_t n = g->n;
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
+  if (bits_written) *bits_written = false;
+  const bool want_bits = relu_bits && L->act == GCN_ACT_RELU;
   if (order == GCN_AGGREGATE_FIRST) {
     // P = S H_in (kept for the backward pass), then H_out = act(P W + b): one fused
     // kernel when the widths allow it (bf16x6 mode, linear S), else an aggregation and a
@@ -216,13 +222,19 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
       return GCN_OK;
     }
     q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
+    const bool fused = fusable && agg_gemm_supported(L->f_in, L->ld_in, L->ld_in, Hin, saved);
+    if (want_bits && !fused && gemm_rows_supported(q)) {
+      q.relu_bits = relu_bits;
+      q.ld_relu_bits = relu_bits_words(L->f_out);
+      if (bits_written) *bits_written = true;
+    }
     if (run && L->agg == GCN_AGG_MAX) {
       GCN_TRY(launch_gemm(q, gws, s));
       return GCN_OK;
     }
     if (run) {
       AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in, L->agg);
-      if (fusable && agg_gemm_supported(L->f_in, L->ld_in, L->ld_in, Hin, saved)) {
+      if (fused) {
         GCN_TRY(launch_agg_gemm(p, g->nnz, &g->split, W, L->f_out, L->f_out, b, L->act == GCN_ACT_RELU, Hout,
                                 L->ld_out, aws, s));
       } else {
@@ -240,6 +252,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_out));
   const GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
   void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(q));
+  if (bits_written) *bits_written = want_bits;  // the aggregation epilogue writes them
   if (!run) return GCN_OK;
   if (x) {
     AggParams p{};
@@ -261,6 +274,10 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out, L->agg);
   p.bias = b;
   if (L->act == GCN_ACT_RELU) p.epi = AGG_RELU;
+  if (want_bits) {
+    p.relu_bits = relu_bits;
+    p.ld_relu_bits = relu_bits_words(L->f_out);
+  }
   if (L->act == GCN_ACT_SOFTMAX_CE) {
     p.epi = AGG_SOFTMAX;
     p.labels = labels;
@@ -275,12 +292,17 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   return GCN_OK;
 }
 
+// mask_bits (optional): the bitmask 1[H_in > 0] written by the previous layer's forward;
+// the transform-first input gradient reads it instead of H_in where the row-panel product
+// serves it; *bits_used tells whether it does (set in the sizing pass too).
 gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, const float* Hin,
                      const gcn_sparse_x* x, const float* saved, const float* W, float* dW, float* db,
-                     float* Gprev, Arena& a, hipStream_t s) {
+                     float* Gprev, Arena& a, hipStream_t s, const uint32_t* mask_bits = nullptr,
+                     bool* bits_used = nullptr) {
   const int32_t n = g->n;
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
+  if (bits_used) *bits_used = false;
   void* cws = a.take<char>((int64_t)colsum_workspace(n, L->f_out));
   if (order == GCN_AGGREGATE_FIRST) {
     // Z = P W + b with P = A_hat H_in: dW = P^T G; dP = G W^T; G_prev = (A_hat dP) * 1[H_in > 0]
@@ -322,6 +344,15 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   t.epi = GEMM_MASK;
   t.mask = Hin;
   t.ldmask = L->ld_in;
+  if (mask_bits && Gprev) {
+    GemmParams tb = t;
+    tb.mask_bits = mask_bits;
+    tb.ld_mask_bits = relu_bits_words(L->f_in);
+    if (gemm_rows_supported(tb)) {
+      t = tb;
+      if (bits_used) *bits_used = true;
+    }
+  }
   void* tws = Gprev ? a.take<char>((int64_t)gemm_workspace(t)) : nullptr;
   if (!run) return GCN_OK;
   GCN_TRY(launch_aggregate(graph_agg(g, L->f_out, G, L->ld_out, Q, ldq, agg_transpose(L->agg)), g->nnz,
@@ -513,7 +544,12 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
         !m->mb[l] || !m->vb[l] || (l < L - 1 && !m->act[l]))
       return fail(GCN_E_INVALID, "gcn_epoch: a layer buffer is NULL");
   }
-  // validate every layer call, then plan the workspace as the maximum over the layer calls
+  // Validate every layer call, then plan the workspace: a prefix holding the ReLU
+  // bitmasks that live from a layer's forward to the next layer's backward (kept where the
+  // producing epilogue can write them and that backward can read them), then the maximum
+  // over the layer calls.  The sizing pass runs with a stand-in address for the bits.
+  uint32_t* const probe = reinterpret_cast<uint32_t*>((uintptr_t)256);
+  bool writes[8] = {}, reads[8] = {};
   size_t need = 0;
   for (int l = 0; l < L; ++l) {
     const gcn_layer* ly = &m->layers[l];
@@ -525,29 +561,41 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
     GCN_TRY(validate_bwd(g, ly, m->grad[l], Hin, xl, saved, m->W[l], m->dW[l], m->db[l],
                          l > 0 ? m->grad[l - 1] : nullptr, who));
     Arena pf, pb;
-    GCN_TRY(layer_fwd(g, ly, Hin, xl, m->W[l], m->b[l], Hout, saved, d_labels, d_loss, nullptr, pf, stream));
+    GCN_TRY(layer_fwd(g, ly, Hin, xl, m->W[l], m->b[l], Hout, saved, d_labels, d_loss, nullptr, pf, stream,
+                      l < L - 1 ? probe : nullptr, &writes[l]));
     GCN_TRY(layer_bwd(g, ly, m->grad[l], Hin, xl, saved, m->W[l], m->dW[l], m->db[l],
-                      l > 0 ? m->grad[l - 1] : nullptr, pb, stream));
+                      l > 0 ? m->grad[l - 1] : nullptr, pb, stream, l > 0 ? probe : nullptr, &reads[l]));
     need = std::max(need, std::max(pf.used, pb.used));
   }
+  int64_t bits_at[8];
+  size_t bits_bytes = 0;
+  for (int l = 0; l < L; ++l) {
+    bits_at[l] = -1;
+    if (l < L - 1 && writes[l] && reads[l + 1]) {
+      bits_at[l] = (int64_t)bits_bytes;
+      bits_bytes += (size_t)round_up((int64_t)g->n * relu_bits_words(m->layers[l].f_out) * 4, 256);
+    }
+  }
   bool query = false;
-  GCN_TRY(ws_protocol(d_ws, ws_bytes, need, who, &query));
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, bits_bytes + need, who, &query));
   if (query) return GCN_OK;
+  char* const base = static_cast<char*>(d_ws);
+  auto bits_of = [&](int l) { return bits_at[l] < 0 ? nullptr : reinterpret_cast<uint32_t*>(base + bits_at[l]); };
   for (int l = 0; l < L; ++l) {
     Arena a;
-    a.base = static_cast<char*>(d_ws);
+    a.base = base + bits_bytes;
     const gcn_layer* ly = &m->layers[l];
     GCN_TRY(layer_fwd(g, ly, l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr, m->W[l], m->b[l],
                       l < L - 1 ? m->act[l] : m->grad[l], m->saved ? m->saved[l] : nullptr, d_labels,
-                      d_loss, nullptr, a, stream));
+                      d_loss, nullptr, a, stream, bits_of(l)));
   }
   for (int l = L - 1; l >= 0; --l) {
     Arena a;
-    a.base = static_cast<char*>(d_ws);
+    a.base = base + bits_bytes;
     const gcn_layer* ly = &m->layers[l];
     GCN_TRY(layer_bwd(g, ly, m->grad[l], l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr,
                       m->saved ? m->saved[l] : nullptr, m->W[l], m->dW[l], m->db[l],
-                      l > 0 ? m->grad[l - 1] : nullptr, a, stream));
+                      l > 0 ? m->grad[l - 1] : nullptr, a, stream, l > 0 ? bits_of(l - 1) : nullptr));
   }
   gcn_adam_tensor t[16];
   for (int l = 0; l < L; ++l) {

@@ -552,6 +552,8 @@ size_t gemm_workspace(const GemmParams& p) {
 
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   if (p.m == 0 || p.n == 0) return GCN_OK;
+  if ((p.mask_bits || p.relu_bits) && !gemm_rows_supported(p))
+    return fail(GCN_E_UNSUPPORTED, "gemm: bitmask epilogues need the row-panel product");
   if (gemm_rows_supported(p)) {
     if (!ws) return fail(GCN_E_INVALID, "gemm: the row-panel product needs its workspace");
     char name[64];

@@ -20,15 +20,17 @@
 //  * the four wavefronts of a workgroup (128 rows) share B through LDS one 16-k step at
 //    a time, double-buffered: the next step is read from L2 while the current one
 //    feeds the matrix cores, with one barrier per step; two workgroups share a CU;
-//  * the epilogue (bias, ReLU) stages the accumulators through LDS and writes C in
-//    256-byte row segments with non-temporal stores.
-// Products with the 1[mask > 0] epilogue use the tiled kernel of gemm.hip.
+//  * the epilogue (bias, ReLU, or the input-gradient mask as a bitmask) stages the
+//    accumulators through LDS and writes C in 256-byte row segments with non-temporal
+//    stores; with ReLU it can also write the bitmask 1[C > 0] (one bit per element).
+// Products with an fp32 1[mask > 0] epilogue use the tiled kernel of gemm.hip.
 // The arithmetic per product is that of gemm.hip's bf16x6 mode (the same six part
 // products, fp32 accumulation), summed in a different order.
 #include <cstdlib>
 #include <cstring>
 
 #include "bf16x6.h"
+#include "lanes.h"
 
 namespace gcn {
 namespace {
@@ -247,30 +249,46 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
     // the fence keeps the compiler from reordering them
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int64_t col = (int64_t)j0 * 32 + sc;
-    if (col < p.n) {
-      const bool full = col + 4 <= p.n;
-      float bias[4] = {0.f, 0.f, 0.f, 0.f};
-      if (p.bias)
+    const bool cin = col < p.n, full = col + 4 <= p.n;
+    float bias[4] = {0.f, 0.f, 0.f, 0.f};
+    if (p.bias && cin)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) bias[q] = col + q < p.n ? p.bias[col + q] : 0.f;
+      for (int q = 0; q < 4; ++q) bias[q] = col + q < p.n ? p.bias[col + q] : 0.f;
+    // bitmask words: 8 lanes (32 columns) per word; the lanes of a word share the row
+    const int64_t word = col / 32;
+    const int shift = (int)(col % 32);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int64_t row = row0 + sr + 4 * i;
-        if (row >= p.m) continue;
-        const float4 t = *reinterpret_cast<const float4*>(stage + (sr + 4 * i) * kStagePitch + sc);
-        float v[4] = {t.x + bias[0], t.y + bias[1], t.z + bias[2], t.w + bias[3]};
-        if constexpr (EPI == GEMM_RELU)
+    for (int i = 0; i < 8; ++i) {
+      const int64_t row = row0 + sr + 4 * i;
+      const bool rin = row < p.m;  // uniform over the 16 lanes of a row
+      const float4 t = *reinterpret_cast<const float4*>(stage + (sr + 4 * i) * kStagePitch + sc);
+      float v[4] = {t.x + bias[0], t.y + bias[1], t.z + bias[2], t.w + bias[3]};
+      if constexpr (EPI == GEMM_RELU) {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.f);
-        float* cp = p.C + row * p.ldc + col;
-        if (full && r.c_vec) {
-          const f32x4 o = {v[0], v[1], v[2], v[3]};
-          __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(cp));
-        } else {
+        for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.f);
+        if (p.relu_bits) {
+          uint32_t bits = 0;
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            if (col + q < p.n) cp[q] = v[q];
+            if (col + q < p.n && v[q] > 0.f) bits |= 1u << (shift + q);
+          bits = group_or<8>(bits);
+          if (rin && cin && l % 8 == 0) p.relu_bits[row * p.ld_relu_bits + word] = bits;
         }
+      }
+      if constexpr (EPI == GEMM_MASK) {
+        const uint32_t mw = rin && cin ? p.mask_bits[row * p.ld_mask_bits + word] >> shift : 0u;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = (mw >> q) & 1u ? v[q] : 0.f;
+      }
+      if (!rin || !cin) continue;
+      float* cp = p.C + row * p.ldc + col;
+      if (full && r.c_vec) {
+        const f32x4 o = {v[0], v[1], v[2], v[3]};
+        __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(cp));
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (col + q < p.n) cp[q] = v[q];
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // before the next pair's writes
@@ -282,6 +300,7 @@ void launch_nj(const RowsArgs& r, hipStream_t s) {
   const dim3 grid((unsigned)ceil_div(r.p.m, kRowsPerBlock));
   switch (r.p.epi) {
     case GEMM_RELU: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_RELU>), grid, dim3(kThreads), 0, s, r); break;
+    case GEMM_MASK: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_MASK>), grid, dim3(kThreads), 0, s, r); break;
     default: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_NONE>), grid, dim3(kThreads), 0, s, r);
   }
 }
@@ -298,10 +317,10 @@ static bool rows_enabled() {
   return !(e && strcmp(e, "0") == 0);
 }
 
-// Products with the mask epilogue (the input gradient) stay on the tiled kernel, measured
-// faster there on the arxiv-like shapes.
+// The mask epilogue runs here only in its bitmask form: with an fp32 mask (a 4-byte read
+// per output) the tiled kernel was measured faster on the arxiv-like shapes.
 bool gemm_rows_supported(const GemmParams& p) {
-  return gemm_bf16x6_mode() && rows_enabled() && p.epi != GEMM_MASK && !p.ta && p.n > 0 && p.n <= 256 && p.k > 0 && p.m >= kRowsPerBlock &&
+  return gemm_bf16x6_mode() && rows_enabled() && (p.epi != GEMM_MASK || p.mask_bits) && !p.ta && p.n > 0 && p.n <= 256 && p.k > 0 && p.m >= kRowsPerBlock &&
          p.lda % 4 == 0 && aligned16(p.A);
 }
 

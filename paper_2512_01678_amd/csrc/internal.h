@@ -97,7 +97,12 @@ struct AggParams {
   int64_t ldl;
   float inv_n;             // 1 / n
   const char* tag;         // kernel family name for the profiler (NULL: derived)
+  // AGG_RELU: optional bitmask of the output, bit c % 32 of word c / 32 of a row = 1[Z > 0]
+  uint32_t* relu_bits;
+  int64_t ld_relu_bits;    // words per row (>= ceil(w / 32))
 };
+// Words per row of a ReLU bitmask of width w.
+inline int64_t relu_bits_words(int32_t w) { return (w + 31) / 32; }
 // Z over all rows; rows longer than GCN_SPLIT_MIN go through the split plan when one
 // is given (its chunk sums live in ws, aggregate_workspace() bytes).
 size_t aggregate_workspace(const gcn_split* split, int32_t w);
@@ -152,6 +157,12 @@ struct GemmParams {
   int32_t epi;
   const float* mask;
   int64_t ldmask;
+  // Bitmask forms (row-panel product only): GEMM_MASK reads bit c % 32 of word c / 32 of
+  // row r of mask_bits instead of mask > 0; GEMM_RELU also writes 1[C > 0] to relu_bits.
+  const uint32_t* mask_bits = nullptr;
+  int64_t ld_mask_bits = 0;
+  uint32_t* relu_bits = nullptr;
+  int64_t ld_relu_bits = 0;
 };
 // Workspace of launch_gemm: split-k partials (A^T B), or the split B of the row-panel
 // product (A B, A B^T with n <= 256); 0 when neither applies.

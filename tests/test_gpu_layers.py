@@ -279,6 +279,37 @@ def tiny(G, orc):
     return Problem(G, orc, wl)
 
 
+@pytest.fixture(scope="module")
+def hubs(G, orc):
+    """20,000 nodes with four rows longer than the split threshold, hidden widths 40 and 24
+    (bitmask rows of a word and a half, and of a partial word)."""
+    wl = gs.Workload("hub_epochs", 20000, "chung_lu", 60000, (48, 40, 24, 8), "normal", 1.0)
+    p = Problem.__new__(Problem)
+    p.wl = wl
+    rng = np.random.default_rng(9)
+    s1, d1 = gs.chung_lu(wl.n, 60000, seed=5)
+    ss, dd = [s1], [d1]
+    for h, k in [(3, 15000), (11, 5000), (12, 4000), (19999, 4200)]:
+        ss.append(np.full(k, h, np.int32))
+        dd.append(rng.choice(wl.n, k, replace=False).astype(np.int32))
+    s, d = np.concatenate(ss), np.concatenate(dd)
+    p.og = orc.build_csr(wl.n, s, d)
+    p.dg = G.build_csr(wl.n, dev(s), dev(d))
+    assert p.dg.n_long >= 3
+    p.X = gs.make_features(wl, 0)
+    p.y = gs.make_labels(wl, 0)
+    p.Ws, p.bs = gs.make_weights(wl, 0)
+    return p
+
+
+def test_epochs_with_hub_rows(G, orc, hubs):
+    """Whole epochs on a graph with split hub rows: the ReLU bitmasks come from the row-panel
+    GEMM epilogue (aggregate-first layer 0), the aggregation epilogue including its long-row
+    combine (transform-first layer 1), and feed both input-gradient products."""
+    m = run_epochs(G, orc, hubs, 2, sparse=False)
+    assert m.orders() == [G.AGGREGATE_FIRST, G.TRANSFORM_FIRST, G.TRANSFORM_FIRST]
+
+
 @pytest.mark.parametrize("aggs", [("sum", "mean", "gcn"), ("max", "sum", "mean"), ("mean", "max", "max")])
 def test_epochs_other_aggregators(G, orc, tiny, aggs):
     """Whole epochs with sum, mean and max layers (the max loss layer goes through the
