@@ -346,8 +346,8 @@ def main():
                    "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
                    "aggregator": args.agg, "x_csc": sparse and args.csc == "on",
                    "timed_events": dominant, "hip_graph": bool(args.graph),
-                   "af_layer": "fused kernel" if os.environ.get("GCN_AF_FUSED") == "1"
-                   else "aggregation + row-panel GEMM",
+                   "af_layer": None if G.AGGREGATE_FIRST not in m.orders() else
+                   "fused kernel" if os.environ.get("GCN_AF_FUSED") == "1" else "aggregation + GEMM",
                    "gemm_mode": "fp32 MFMA" if os.environ.get("GCN_GEMM_MODE") == "fp32"
                    else "fp32 via exact 3-way bf16 split, 6 bf16 MFMA products"},
         "roofline": roofline, "cpu_baseline": cpu, "spmm": spmm, "memory": memory, "kernels": kernels,

@@ -343,9 +343,9 @@ gcn_status gcn_aggregate_max_bwd(const gcn_graph* g, int32_t w, const float* d_d
  * GCN_EPI_MASK with d_mask m x n, pitch ldmask).  GCN_OP_TN may split k across
  * workgroups; its partial products live in the workspace and are summed in a
  * fixed order.  GCN_OP_NN / GCN_OP_NT without the mask epilogue, n <= 256 and
- * m >= 128 (A 16-byte aligned, lda % 4 == 0) split B once into the workspace
- * (3 bf16 planes, about 6 k n bytes) and stream the rows of A; the workspace is
- * then required.
+ * m >= 32768 (A 16-byte aligned, lda % 4 == 0; GCN_GEMM_ROWS=1 from m >= 128 on,
+ * =0 never) split B once into the workspace (3 bf16 planes, about 6 k n bytes)
+ * and stream the rows of A; the workspace is then required.
  */
 gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_A, int64_t lda,
                     const float* d_B, int64_t ldb, float* d_C, int64_t ldc, const float* d_bias,

@@ -311,16 +311,23 @@ int64_t split_b_elems(const GemmParams& p) {
 
 }  // namespace
 
-// GCN_GEMM_ROWS=0 sends these products to the general tiled kernel (for comparison).
-static bool rows_enabled() {
+// Below this many rows the extra launch of the weight split costs more than the
+// row-panel kernel saves (a Cora-sized epoch is launch-latency bound).
+constexpr int64_t kRowsAuto = 32768;
+
+// GCN_GEMM_ROWS=0 sends these products to the general tiled kernel, =1 takes the
+// row-panel kernel whatever the row count; unset: from kRowsAuto rows on.
+static bool rows_enabled(int64_t m) {
   const char* e = getenv("GCN_GEMM_ROWS");
-  return !(e && strcmp(e, "0") == 0);
+  if (e && strcmp(e, "0") == 0) return false;
+  if (e && strcmp(e, "1") == 0) return true;
+  return m >= kRowsAuto;
 }
 
 // The mask epilogue runs here only in its bitmask form: with an fp32 mask (a 4-byte read
 // per output) the tiled kernel was measured faster on the arxiv-like shapes.
 bool gemm_rows_supported(const GemmParams& p) {
-  return gemm_bf16x6_mode() && rows_enabled() && (p.epi != GEMM_MASK || p.mask_bits) && !p.ta && p.n > 0 && p.n <= 256 && p.k > 0 && p.m >= kRowsPerBlock &&
+  return gemm_bf16x6_mode() && rows_enabled(p.m) && (p.epi != GEMM_MASK || p.mask_bits) && !p.ta && p.n > 0 && p.n <= 256 && p.k > 0 && p.m >= kRowsPerBlock &&
          p.lda % 4 == 0 && aligned16(p.A);
 }
 

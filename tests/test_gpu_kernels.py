@@ -303,7 +303,8 @@ ROWS_CASES = [(256, 1, 5), (1000, 33, 32), (4099, 64, 40), (777, 65, 256), (300,
 
 @pytest.mark.parametrize("op", ["NN", "NT"])
 @pytest.mark.parametrize("shape", ROWS_CASES, ids=lambda s: "x".join(map(str, s)))
-def test_gemm_row_panels(G, op, shape):
+def test_gemm_row_panels(G, op, shape, monkeypatch):
+    monkeypatch.setenv("GCN_GEMM_ROWS", "1")  # below the automatic row threshold
     m, n, k = shape
     rng = np.random.default_rng(m + 3 * n + 7 * k)
     A = (rng.standard_normal((m, k)) * np.exp(rng.standard_normal((m, 1)))).astype(np.float32)

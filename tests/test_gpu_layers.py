@@ -267,7 +267,11 @@ def test_epochs_sparse_path_atomic_transpose(G, orc, cora):
     assert m.step == 2
 
 
-def test_epochs_dense_path_aggregate_first(G, orc, small):
+@pytest.mark.parametrize("rows", ["auto", "1"])
+def test_epochs_dense_path_aggregate_first(G, orc, small, rows, monkeypatch):
+    """rows=1: the row-panel products and the ReLU bitmasks below their automatic threshold."""
+    if rows != "auto":
+        monkeypatch.setenv("GCN_GEMM_ROWS", rows)
     m = run_epochs(G, orc, small, 2, sparse=False)
     assert m.orders()[0] == G.AGGREGATE_FIRST and m.orders()[1] == G.TRANSFORM_FIRST
 
@@ -302,10 +306,12 @@ def hubs(G, orc):
     return p
 
 
-def test_epochs_with_hub_rows(G, orc, hubs):
+def test_epochs_with_hub_rows(G, orc, hubs, monkeypatch):
     """Whole epochs on a graph with split hub rows: the ReLU bitmasks come from the row-panel
     GEMM epilogue (aggregate-first layer 0), the aggregation epilogue including its long-row
-    combine (transform-first layer 1), and feed both input-gradient products."""
+    combine (transform-first layer 1), and feed both input-gradient products (row-panel
+    products forced below their automatic row threshold)."""
+    monkeypatch.setenv("GCN_GEMM_ROWS", "1")
     m = run_epochs(G, orc, hubs, 2, sparse=False)
     assert m.orders() == [G.AGGREGATE_FIRST, G.TRANSFORM_FIRST, G.TRANSFORM_FIRST]
 
