@@ -294,15 +294,19 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
 
 // mask_bits (optional): the bitmask 1[H_in > 0] written by the previous layer's forward;
 // the transform-first input gradient reads it instead of H_in where the row-panel product
-// serves it; *bits_used tells whether it does (set in the sizing pass too).
+// serves it; *bits_used tells whether it does (set in the sizing pass too).  On that path
+// the product also writes the column sums of G_prev into db_prev when given (the bias
+// gradient of the layer below; *db_prev_done).  db_ready: db was written that way already.
 gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, const float* Hin,
                      const gcn_sparse_x* x, const float* saved, const float* W, float* dW, float* db,
                      float* Gprev, Arena& a, hipStream_t s, const uint32_t* mask_bits = nullptr,
-                     bool* bits_used = nullptr) {
+                     bool* bits_used = nullptr, float* db_prev = nullptr, bool* db_prev_done = nullptr,
+                     bool db_ready = false) {
   const int32_t n = g->n;
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
   if (bits_used) *bits_used = false;
+  if (db_prev_done) *db_prev_done = false;
   void* cws = a.take<char>((int64_t)colsum_workspace(n, L->f_out));
   if (order == GCN_AGGREGATE_FIRST) {
     // Z = P W + b with P = A_hat H_in: dW = P^T G; dP = G W^T; G_prev = (A_hat dP) * 1[H_in > 0]
@@ -315,7 +319,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     void* tws = Gprev ? a.take<char>((int64_t)gemm_workspace(t)) : nullptr;
     if (!run) return GCN_OK;
     GCN_TRY(launch_gemm(dw, gws, s));
-    GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
+    if (!db_ready) GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
     if (Gprev) {
       GCN_TRY(launch_gemm(t, tws, s));
       AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in, agg_transpose(L->agg));
@@ -351,6 +355,10 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     if (gemm_rows_supported(tb)) {
       t = tb;
       if (bits_used) *bits_used = true;
+      if (db_prev) {
+        t.colsum = db_prev;
+        if (db_prev_done) *db_prev_done = true;
+      }
     }
   }
   void* tws = Gprev ? a.take<char>((int64_t)gemm_workspace(t)) : nullptr;
@@ -377,7 +385,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   } else {
     GCN_TRY(launch_gemm(dw, gws, s));
   }
-  GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
+  if (!db_ready) GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
   if (Gprev) GCN_TRY(launch_gemm(t, tws, s));
   return GCN_OK;
 }
@@ -549,7 +557,8 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
   // producing epilogue can write them and that backward can read them), then the maximum
   // over the layer calls.  The sizing pass runs with a stand-in address for the bits.
   uint32_t* const probe = reinterpret_cast<uint32_t*>((uintptr_t)256);
-  bool writes[8] = {}, reads[8] = {};
+  float* const probe_db = reinterpret_cast<float*>((uintptr_t)256);
+  bool writes[8] = {}, reads[8] = {}, sums[8] = {};  // sums[l]: layer l's backward can write db[l-1]
   size_t need = 0;
   for (int l = 0; l < L; ++l) {
     const gcn_layer* ly = &m->layers[l];
@@ -564,7 +573,8 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
     GCN_TRY(layer_fwd(g, ly, Hin, xl, m->W[l], m->b[l], Hout, saved, d_labels, d_loss, nullptr, pf, stream,
                       l < L - 1 ? probe : nullptr, &writes[l]));
     GCN_TRY(layer_bwd(g, ly, m->grad[l], Hin, xl, saved, m->W[l], m->dW[l], m->db[l],
-                      l > 0 ? m->grad[l - 1] : nullptr, pb, stream, l > 0 ? probe : nullptr, &reads[l]));
+                      l > 0 ? m->grad[l - 1] : nullptr, pb, stream, l > 0 ? probe : nullptr, &reads[l],
+                      l > 0 ? probe_db : nullptr, &sums[l]));
     need = std::max(need, std::max(pf.used, pb.used));
   }
   int64_t bits_at[8];
@@ -589,13 +599,19 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
                       l < L - 1 ? m->act[l] : m->grad[l], m->saved ? m->saved[l] : nullptr, d_labels,
                       d_loss, nullptr, a, stream, bits_of(l)));
   }
+  // with the bitmask, layer l's input-gradient product also sums the columns of G_{l-1}
+  // (db of layer l - 1), which then skips its own column-sum pass over G_{l-1}
+  bool db_from_above[8] = {};
   for (int l = L - 1; l >= 0; --l) {
     Arena a;
     a.base = base + bits_bytes;
     const gcn_layer* ly = &m->layers[l];
+    const bool fuse_db = l > 0 && bits_at[l - 1] >= 0 && sums[l];
     GCN_TRY(layer_bwd(g, ly, m->grad[l], l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr,
                       m->saved ? m->saved[l] : nullptr, m->W[l], m->dW[l], m->db[l],
-                      l > 0 ? m->grad[l - 1] : nullptr, a, stream, l > 0 ? bits_of(l - 1) : nullptr));
+                      l > 0 ? m->grad[l - 1] : nullptr, a, stream, l > 0 ? bits_of(l - 1) : nullptr, nullptr,
+                      fuse_db ? m->db[l - 1] : nullptr, nullptr, db_from_above[l]));
+    if (fuse_db) db_from_above[l - 1] = true;
   }
   gcn_adam_tensor t[16];
   for (int l = 0; l < L; ++l) {

@@ -42,6 +42,7 @@ constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kSlab = 32;          // k per slab: two 32x32x16 steps
 constexpr int kBlockBf16 = 64 * 8;  // one fragment block: 64 lanes x 8 bf16 (1 KB)
 constexpr int kStagePitch = 64 + 4;   // floats per staged epilogue row
+constexpr int kMaxN = 256;            // output columns served
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -54,6 +55,7 @@ struct RowsArgs {
   int nj;            // column tiles (ceil(n / 32))
   int64_t nslab;
   int c_vec;         // C rows 16-byte aligned with ldc % 4 == 0
+  float* part;       // p.colsum: per-workgroup column sums [workgroups][n]
 };
 
 // One thread per (slab, step, column tile, lane): 8 values of B, split into 3 planes.
@@ -107,7 +109,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   constexpr int kChunks = kStepBf16 / 8;          // 16-byte pieces per step
   constexpr int kPer = (kChunks + kThreads - 1) / kThreads;
   // two B steps during the k walk, then the epilogue staging (32 x 68 floats per wave)
-  constexpr int kStageBf16 = 2 * kWaves * kRowsPerWave * kStagePitch;
+  // (+ the wavefronts' column sums of the mask epilogue)
+  constexpr int kStageBf16 = 2 * kWaves * kRowsPerWave * kStagePitch + (EPI == GEMM_MASK ? 2 * kWaves * kMaxN : 0);
   constexpr int kLdsBf16 = 2 * kStepBf16 > kStageBf16 ? 2 * kStepBf16 : kStageBf16;
   __shared__ __attribute__((aligned(16))) __bf16 lds[kLdsBf16];
 
@@ -257,6 +260,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
     // bitmask words: 8 lanes (32 columns) per word; the lanes of a word share the row
     const int64_t word = col / 32;
     const int shift = (int)(col % 32);
+    float cs[4] = {0.f, 0.f, 0.f, 0.f};  // column sums of this lane's rows (mask epilogue)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int64_t row = row0 + sr + 4 * i;
@@ -278,7 +282,10 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
       if constexpr (EPI == GEMM_MASK) {
         const uint32_t mw = rin && cin ? p.mask_bits[row * p.ld_mask_bits + word] >> shift : 0u;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = (mw >> q) & 1u ? v[q] : 0.f;
+        for (int q = 0; q < 4; ++q) {
+          v[q] = (mw >> q) & 1u ? v[q] : 0.f;
+          cs[q] += v[q];  // rows past m have mw = 0
+        }
       }
       if (!rin || !cin) continue;
       float* cp = p.C + row * p.ldc + col;
@@ -291,7 +298,36 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
           if (col + q < p.n) cp[q] = v[q];
       }
     }
+    if constexpr (EPI == GEMM_MASK) {
+      if (r.part) {
+        // the four lanes of a column (rows sr = 0..3) in a fixed order, then one partial
+        // row of this wavefront's 32 rows
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          cs[q] += __shfl_xor(cs[q], 16, 64);
+          cs[q] += __shfl_xor(cs[q], 32, 64);
+        }
+        float* ws = reinterpret_cast<float*>(lds) + kWaves * kRowsPerWave * kStagePitch + wave * kMaxN + col;
+        if (sr == 0 && cin)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (col + q < p.n) ws[q] = cs[q];
+      }
+    }
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // before the next pair's writes
+  }
+  if constexpr (EPI == GEMM_MASK) {
+    if (r.part) {
+      // the workgroup's partial row: the wavefronts' sums of column t, in wavefront order
+      __syncthreads();
+      const float* ws = reinterpret_cast<const float*>(lds) + kWaves * kRowsPerWave * kStagePitch;
+      for (int t = tid; t < p.n; t += kThreads) {
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) v += ws[w * kMaxN + t];
+        r.part[(int64_t)blockIdx.x * p.n + t] = v;
+      }
+    }
   }
 }
 
@@ -307,6 +343,11 @@ void launch_nj(const RowsArgs& r, hipStream_t s) {
 
 int64_t split_b_elems(const GemmParams& p) {
   return ceil_div(p.k, kSlab) * 2 * ceil_div(p.n, 32) * 3 * kBlockBf16;
+}
+
+// Partial rows of the fused column sums: one per workgroup.
+int64_t colsum_parts(const GemmParams& p) {
+  return p.colsum && p.epi == GEMM_MASK ? ceil_div(p.m, kRowsPerBlock) : 0;
 }
 
 }  // namespace
@@ -332,7 +373,11 @@ bool gemm_rows_supported(const GemmParams& p) {
 }
 
 size_t gemm_rows_workspace(const GemmParams& p) {
-  return gemm_rows_supported(p) ? sizeof(__bf16) * (size_t)split_b_elems(p) : 0;
+  if (!gemm_rows_supported(p)) return 0;
+  const int64_t parts = colsum_parts(p);
+  return (size_t)round_up((int64_t)sizeof(__bf16) * split_b_elems(p), 256) +
+         (size_t)round_up((int64_t)sizeof(float) * parts * p.n, 256) +
+         (parts ? colsum_workspace(parts, (int32_t)p.n) : 0);
 }
 
 gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
@@ -342,6 +387,10 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
   r.nslab = ceil_div(p.k, kSlab);
   r.bp = static_cast<const __bf16*>(ws);
   r.c_vec = p.ldc % 4 == 0 && aligned16(p.C);
+  const int64_t nparts = colsum_parts(p);
+  r.part = nparts ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                             round_up((int64_t)sizeof(__bf16) * split_b_elems(p), 256))
+                  : nullptr;
   const int64_t threads = r.nslab * 2 * r.nj * 64;
   hipLaunchKernelGGL(k_split_b, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, s, r, threads,
                      static_cast<__bf16*>(ws));
@@ -356,7 +405,11 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
     case 7: launch_nj<7, 1>(r, s); break;
     default: launch_nj<8, 1>(r, s);
   }
-  return check_launch("gemm (row panels)");
+  GCN_TRY(check_launch("gemm (row panels)"));
+  if (!nparts) return GCN_OK;
+  // the partial rows are a small matrix: its column sums by the two-level fixed-order pass
+  void* cws = reinterpret_cast<char*>(r.part) + round_up((int64_t)sizeof(float) * nparts * p.n, 256);
+  return launch_colsum(nparts, (int32_t)p.n, r.part, p.n, p.colsum, nullptr, nullptr, cws, s);
 }
 
 }  // namespace gcn

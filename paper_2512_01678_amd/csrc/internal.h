@@ -163,6 +163,9 @@ struct GemmParams {
   int64_t ld_mask_bits = 0;
   uint32_t* relu_bits = nullptr;
   int64_t ld_relu_bits = 0;
+  // Row-panel product with GEMM_MASK only: also write the column sums of C (n floats,
+  // fixed order) -- the bias gradient of the layer below, whose gradient C is.
+  float* colsum = nullptr;
 };
 // Workspace of launch_gemm: split-k partials (A^T B), or the split B of the row-panel
 // product (A B, A B^T with n <= 256); 0 when neither applies.
