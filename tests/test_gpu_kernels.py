@@ -353,6 +353,25 @@ def test_gemm_row_panels_full_size(G, op, n, k, epi):
     assert_mag_close(host(C[rows]), ref, mag, f"rows {op} full size {n}x{k}")
 
 
+@pytest.mark.parametrize("m,n,k", [(1, 1, 17), (33, 40, 1000), (256, 256, 5000), (100, 256, 70001),
+                                   (256, 40, 50000), (200, 7, 33333), (64, 256, 123), (160, 96, 65)])
+def test_gemm_tn_ragged(G, m, n, k):
+    """A^T B on ragged output tiles, partial k slabs and split-k ranges (with a bias)."""
+    rng = np.random.default_rng(m * 31 + n + k)
+    A = (rng.standard_normal((k, m)) * np.exp(rng.standard_normal((k, 1)))).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    bias = rng.standard_normal(n).astype(np.float32)
+    ref = A.T.astype(np.float64) @ B.astype(np.float64) + bias
+    mag = np.abs(A.T.astype(np.float64)) @ np.abs(B.astype(np.float64)) + np.abs(bias)
+    Ad, Bd = pitched(A, G.pitch(m) + 4), pitched(B, G.pitch(n))
+    C = pitched(np.full((m, n), np.nan, np.float32), G.pitch(n))
+    G.gemm(G.OP_TN, Ad, Bd, C, bias=dev(bias))
+    C1 = host(C).copy()
+    assert_mag_close(C1, ref, mag, f"TN ragged {m}x{n}x{k}")
+    G.gemm(G.OP_TN, Ad, Bd, C, bias=dev(bias))
+    np.testing.assert_array_equal(host(C), C1)  # fixed-order reduction
+
+
 # ---------------------------------------------------------------------------
 # bias gradient / loss mean, Adam
 # ---------------------------------------------------------------------------

@@ -522,6 +522,31 @@ def test_hip_graph_replay_matches_eager(G, small):
     assert graphed.step == eager.step == 3
 
 
+def test_epoch_graph_replays_match_eager(G, small):
+    """An epoch captured in a HIP graph replayed three times, with eager work between the
+    replays, against an identical model stepped eagerly: equal bit for bit each time."""
+    p = small
+    n = p.wl.n
+    Xd, yd = dev(p.X), dev(p.y)
+    a = G.Model(n, p.wl.widths, p.Ws, p.bs, device_step=True)
+    b = G.Model(n, p.wl.widths, p.Ws, p.bs, device_step=True)
+    a.prepare(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        a.epoch_captured(p.dg, X=Xd, labels=yd)
+    torch.cuda.synchronize()
+    for r in range(3):
+        graph.replay()
+        b.epoch(p.dg, X=Xd, labels=yd)
+        torch.cuda.synchronize()
+        for x, y in zip(a.W + a.b + a.dW + a.db, b.W + b.b + b.dW + b.db):
+            np.testing.assert_array_equal(host(x), host(y), err_msg=f"replay {r}")
+        np.testing.assert_array_equal(host(a.loss), host(b.loss))
+        filler = torch.randn(4096, device="cuda")  # eager work between replays
+        assert torch.isfinite(filler.sum())
+
+
 def test_device_step_matches_host_step(G, small):
     p = small
     n = p.wl.n
