@@ -470,6 +470,10 @@ Shape pick_shape(const GemmParams& p, bool emu) {
   const int bm = emu ? 128 : 256;
   if (p.n <= 32) return {bm, 32};
   if (p.n <= 64) return {bm, 64};
+  // A^T B (weight gradients, split k) with both sides above 128: one 256 x 256 tile
+  // (8 wavefronts) reads each operand once instead of twice (arxiv-like 256 x 256:
+  // 142 -> 126 us; a 128 x 256 tile for the 128-wide case was slower than 128 x 128)
+  if (p.ta && emu && p.n > 128 && p.m > 128) return {256, 256};
   return {128, 128};
 }
 
@@ -478,7 +482,7 @@ int64_t pick_splits(const GemmParams& p, Shape sh) {
   // about 2048 wavefronts in all (measured best for wide and narrow tiles alike), each
   // workgroup walking at least 256 rows of k
   const int64_t tiles = ceil_div(p.m, sh.bm) * ceil_div(p.n, sh.bn);
-  const int64_t waves = sh.bn >= 128 ? 4 : sh.bm / 64;
+  const int64_t waves = sh.bn >= 256 ? 8 : (sh.bn >= 128 ? 4 : sh.bm / 64);
   int64_t s = ceil_div(2048, tiles * waves);
   const int64_t max_s = ceil_div(p.k, 256);
   if (s > max_s) s = max_s;
@@ -514,6 +518,9 @@ gcn_status launch_shape(const GemmArgs& g, Shape sh, int64_t splits, hipStream_t
   constexpr int BMN = EMU ? 128 : 256, WMN = BMN / 64;
   if (sh.bn == 32) return launch_tile<BMN, 32, 16, WMN, 1, TA, TB, EMU>(g, splits, s);
   if (sh.bn == 64) return launch_tile<BMN, 64, 16, WMN, 1, TA, TB, EMU>(g, splits, s);
+  if constexpr (TA && !TB && EMU) {
+    if (sh.bn == 256) return launch_tile<256, 256, 16, 2, 4, TA, TB, EMU>(g, splits, s);
+  }
   return launch_tile<128, 128, BKW, 2, 2, TA, TB, EMU>(g, splits, s);
 }
 
