@@ -157,10 +157,20 @@ GemmParams gemm(int64_t m, int64_t n, int64_t k, const float* A, int64_t lda, bo
 // relu_bits (optional, ReLU layers): also write the bitmask 1[H_out > 0] (relu_bits_words
 // words per row) where the producing kernel can; *bits_written tells whether it does (set
 // in the sizing pass too).
+// The mean of the per-row losses; with db_out, the same fixed-order pass also sums the
+// columns of G = dLoss/dZ (written to Hout by the loss epilogue), the layer's bias gradient,
+// so that the backward pass need not read G again for it.
+gcn_status loss_pass(int32_t n, const gcn_layer* L, const float* G, const float* row_loss, float* loss,
+                     float* db_out, void* cws, hipStream_t s) {
+  if (db_out) return launch_colsum(n, L->f_out, G, L->ld_out, db_out, row_loss, loss, cws, s);
+  return launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s);
+}
+
 gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, const gcn_sparse_x* x,
                      const float* W, const float* b, float* Hout, float* saved, const int32_t* labels,
                      float* loss, float* logits, Arena& a, hipStream_t s, uint32_t* relu_bits = nullptr,
-                     bool* bits_written = nullptr) {
+                     bool* bits_written = nullptr, float* db_out = nullptr, const SplitJob* sj = nullptr,
+                     int nsj = 0) {
   const int32_t n = g->n;
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
@@ -182,7 +192,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     int64_t* id_ptr = softmax ? a.take<int64_t>((int64_t)n + 1) : nullptr;
     int32_t* id_col = softmax ? a.take<int32_t>(n) : nullptr;
     float* row_loss = softmax ? a.take<float>(n) : nullptr;
-    void* cws = softmax ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+    void* cws = softmax ? a.take<char>((int64_t)colsum_workspace(n, L->f_out)) : nullptr;
     // H_out = P W (+ b) when the fused kernel does not run (split weight in the workspace)
     GemmParams q = gemm(n, L->f_out, L->f_in, saved, L->ld_in, false, W, L->f_out, false, softmax ? Zs : Hout,
                         softmax ? ldz : L->ld_out);
@@ -198,7 +208,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
         AggParams p = graph_agg(g, L->f_in, Hin, L->ld_in, saved, L->ld_in, L->agg);
         GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
       }
-      GCN_TRY(launch_gemm(q, gws, s));
+      GCN_TRY(launch_gemm(with_split(q, sj, nsj), gws, s));
       GCN_TRY(launch_identity_csr(n, id_ptr, id_col, s));
       AggParams z{};
       z.n = n;
@@ -218,7 +228,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
       z.inv_n = n > 0 ? 1.f / (float)n : 0.f;
       z.tag = "softmax_ce";
       GCN_TRY(launch_aggregate(z, n, nullptr, nullptr, s));
-      GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
+      GCN_TRY(loss_pass(n, L, Hout, row_loss, loss, db_out, cws, s));
       return GCN_OK;
     }
     q.epi = L->act == GCN_ACT_RELU ? GEMM_RELU : GEMM_NONE;
@@ -229,7 +239,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
       if (bits_written) *bits_written = true;
     }
     if (run && L->agg == GCN_AGG_MAX) {
-      GCN_TRY(launch_gemm(q, gws, s));
+      GCN_TRY(launch_gemm(with_split(q, sj, nsj), gws, s));
       return GCN_OK;
     }
     if (run) {
@@ -239,7 +249,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
                                 L->ld_out, aws, s));
       } else {
         GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
-        GCN_TRY(launch_gemm(q, gws, s));
+        GCN_TRY(launch_gemm(with_split(q, sj, nsj), gws, s));
       }
     }
     return GCN_OK;
@@ -248,7 +258,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   const int64_t ldm = pitch4(L->f_out);
   float* M = a.take<float>((int64_t)n * ldm);
   float* row_loss = L->act == GCN_ACT_SOFTMAX_CE ? a.take<float>(n) : nullptr;
-  void* cws = L->act == GCN_ACT_SOFTMAX_CE ? a.take<char>((int64_t)colsum_workspace(n, 0)) : nullptr;
+  void* cws = L->act == GCN_ACT_SOFTMAX_CE ? a.take<char>((int64_t)colsum_workspace(n, L->f_out)) : nullptr;
   void* aws = a.take<char>((int64_t)aggregate_workspace(&g->split, L->f_out));
   const GemmParams q = gemm(n, L->f_out, L->f_in, Hin, L->ld_in, false, W, L->f_out, false, M, ldm);
   void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(q));
@@ -269,7 +279,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.tag = "spmm_xw";
     GCN_TRY(launch_aggregate(p, x->nnz, nullptr, nullptr, s));
   } else {
-    GCN_TRY(launch_gemm(q, gws, s));
+    GCN_TRY(launch_gemm(with_split(q, sj, nsj), gws, s));
   }
   AggParams p = graph_agg(g, L->f_out, M, ldm, Hout, L->ld_out, L->agg);
   p.bias = b;
@@ -287,8 +297,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
     p.inv_n = n > 0 ? 1.f / (float)n : 0.f;
   }
   GCN_TRY(launch_aggregate(p, g->nnz, &g->split, aws, s));
-  if (L->act == GCN_ACT_SOFTMAX_CE)
-    GCN_TRY(launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s));
+  if (L->act == GCN_ACT_SOFTMAX_CE) GCN_TRY(loss_pass(n, L, Hout, row_loss, loss, db_out, cws, s));
   return GCN_OK;
 }
 
@@ -301,7 +310,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
                      const gcn_sparse_x* x, const float* saved, const float* W, float* dW, float* db,
                      float* Gprev, Arena& a, hipStream_t s, const uint32_t* mask_bits = nullptr,
                      bool* bits_used = nullptr, float* db_prev = nullptr, bool* db_prev_done = nullptr,
-                     bool db_ready = false) {
+                     bool db_ready = false, const SplitJob* sj = nullptr, int nsj = 0) {
   const int32_t n = g->n;
   const int32_t order = resolve_order(L, x != nullptr);
   const bool run = a.base != nullptr;
@@ -321,7 +330,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     GCN_TRY(launch_gemm(dw, gws, s));
     if (!db_ready) GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
     if (Gprev) {
-      GCN_TRY(launch_gemm(t, tws, s));
+      GCN_TRY(launch_gemm(with_split(t, sj, nsj), tws, s));
       AggParams p = graph_agg(g, L->f_in, T, ldt, Gprev, L->ld_in, agg_transpose(L->agg));
       if (L->agg == GCN_AGG_MAX) {
         // each (G W^T)[v,c] goes back to the saved maximiser of (v, c)
@@ -386,7 +395,7 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     GCN_TRY(launch_gemm(dw, gws, s));
   }
   if (!db_ready) GCN_TRY(launch_colsum(n, L->f_out, G, L->ld_out, db, nullptr, nullptr, cws, s));
-  if (Gprev) GCN_TRY(launch_gemm(t, tws, s));
+  if (Gprev) GCN_TRY(launch_gemm(with_split(t, sj, nsj), tws, s));
   return GCN_OK;
 }
 
@@ -586,22 +595,49 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
       bits_bytes += (size_t)round_up((int64_t)g->n * relu_bits_words(m->layers[l].f_out) * 4, 256);
     }
   }
+  // Every weight in the two forms the row-panel products take it in (W for H W, W^T for
+  // the input gradient), split once at the start: the weights change only in the Adam
+  // step at the end.  A product that does not take the row-panel kernel ignores its job.
+  SplitJob jobs[kMaxSplitJobs];
+  int njobs = 0;
+  int64_t job_at[kMaxSplitJobs];
+  for (int l = 0; l < L; ++l) {
+    const int64_t fi = m->layers[l].f_in, fo = m->layers[l].f_out;
+    const float* const aligned_probe = reinterpret_cast<const float*>((uintptr_t)256);
+    for (int form = 0; form < 2; ++form) {
+      const bool tb = form == 1;
+      if (tb && l == 0) continue;           // no input gradient below layer 0
+      if (!tb && l == 0 && x) continue;     // sparse X: the first product is X_csr W
+      const int64_t k = tb ? fo : fi, n = tb ? fi : fo;
+      const GemmParams probe = gemm(g->n, n, k, aligned_probe, round_up(k, 4), false, m->W[l], fo, tb, nullptr, n);
+      if (!gemm_rows_supported(probe) || njobs == kMaxSplitJobs) continue;
+      jobs[njobs] = SplitJob{m->W[l], fo, tb, k, n, nullptr};
+      job_at[njobs] = (int64_t)bits_bytes;
+      bits_bytes += gemm_rows_split_bytes(jobs[njobs]);
+      ++njobs;
+    }
+  }
   bool query = false;
   GCN_TRY(ws_protocol(d_ws, ws_bytes, bits_bytes + need, who, &query));
   if (query) return GCN_OK;
   char* const base = static_cast<char*>(d_ws);
   auto bits_of = [&](int l) { return bits_at[l] < 0 ? nullptr : reinterpret_cast<uint32_t*>(base + bits_at[l]); };
+  for (int q = 0; q < njobs; ++q) jobs[q].out = base + job_at[q];
+  GCN_TRY(launch_split_batch(jobs, njobs, stream));
   for (int l = 0; l < L; ++l) {
     Arena a;
     a.base = base + bits_bytes;
     const gcn_layer* ly = &m->layers[l];
     GCN_TRY(layer_fwd(g, ly, l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr, m->W[l], m->b[l],
                       l < L - 1 ? m->act[l] : m->grad[l], m->saved ? m->saved[l] : nullptr, d_labels,
-                      d_loss, nullptr, a, stream, bits_of(l)));
+                      d_loss, nullptr, a, stream, bits_of(l), nullptr, l == L - 1 ? m->db[l] : nullptr, jobs,
+                      njobs));
   }
   // with the bitmask, layer l's input-gradient product also sums the columns of G_{l-1}
-  // (db of layer l - 1), which then skips its own column-sum pass over G_{l-1}
+  // (db of layer l - 1), which then skips its own column-sum pass over G_{l-1}; the last
+  // layer's bias gradient comes out of the loss pass of the forward
   bool db_from_above[8] = {};
+  db_from_above[L - 1] = true;
   for (int l = L - 1; l >= 0; --l) {
     Arena a;
     a.base = base + bits_bytes;
@@ -610,7 +646,7 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
     GCN_TRY(layer_bwd(g, ly, m->grad[l], l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr,
                       m->saved ? m->saved[l] : nullptr, m->W[l], m->dW[l], m->db[l],
                       l > 0 ? m->grad[l - 1] : nullptr, a, stream, l > 0 ? bits_of(l - 1) : nullptr, nullptr,
-                      fuse_db ? m->db[l - 1] : nullptr, nullptr, db_from_above[l]));
+                      fuse_db ? m->db[l - 1] : nullptr, nullptr, db_from_above[l], jobs, njobs));
     if (fuse_db) db_from_above[l - 1] = true;
   }
   gcn_adam_tensor t[16];

@@ -58,15 +58,14 @@ struct RowsArgs {
   float* part;       // p.colsum: per-workgroup column sums [workgroups][n]
 };
 
-// One thread per (slab, step, column tile, lane): 8 values of B, split into 3 planes.
-__global__ void __launch_bounds__(256) k_split_b(RowsArgs r, int64_t total, __bf16* out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  const GemmParams& p = r.p;
+// Thread i of a split of B (k x n, or its transpose stored n x k): 8 values of B for one
+// (slab, step, column tile, lane), split into 3 planes.
+__device__ __forceinline__ void split_b_one(const float* B, int64_t ldb, bool tb, int64_t kk, int64_t nn, int nj,
+                                            int64_t i, __bf16* out) {
   const int l = (int)(i % 64);
   const int64_t blk = i / 64;  // (slab * 2 + t) * nj + j
-  const int j = (int)(blk % r.nj);
-  const int64_t st = blk / r.nj;
+  const int j = (int)(blk % nj);
+  const int64_t st = blk / nj;
   const int t = (int)(st % 2);
   const int64_t s = st / 2;
   const int64_t col = (int64_t)j * 32 + l % 32;
@@ -75,7 +74,7 @@ __global__ void __launch_bounds__(256) k_split_b(RowsArgs r, int64_t total, __bf
   for (int e = 0; e < 8; ++e) {
     const int64_t k = s * kSlab + kmap(t, l / 32, e);
     v[e] = 0.f;
-    if (k < p.k && col < p.n) v[e] = p.tb ? p.B[col * p.ldb + k] : p.B[k * p.ldb + col];
+    if (k < kk && col < nn) v[e] = tb ? B[col * ldb + k] : B[k * ldb + col];
   }
   uint4 hi, mid, lo;
   split_pair(v[0], v[1], hi.x, mid.x, lo.x);
@@ -86,6 +85,33 @@ __global__ void __launch_bounds__(256) k_split_b(RowsArgs r, int64_t total, __bf
   o[0] = hi;
   o[64] = mid;
   o[128] = lo;
+}
+
+// Threads of one split: 64 per (slab, step, column tile).
+inline int64_t split_threads(int64_t k, int64_t n) { return ceil_div(k, kSlab) * 2 * ceil_div(n, 32) * 64; }
+
+__global__ void __launch_bounds__(256) k_split_b(RowsArgs r, int64_t total, __bf16* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= total) return;
+  split_b_one(r.p.B, r.p.ldb, r.p.tb, r.p.k, r.p.n, r.nj, i, out);
+}
+
+struct SplitBatch {
+  const float* B[kMaxSplitJobs];
+  __bf16* out[kMaxSplitJobs];
+  int64_t ldb[kMaxSplitJobs], k[kMaxSplitJobs], n[kMaxSplitJobs];
+  int64_t first[kMaxSplitJobs + 1];  // first thread of each job
+  int32_t tb[kMaxSplitJobs], nj[kMaxSplitJobs];
+  int32_t count;
+};
+
+// Every job of the batch in one launch; thread i belongs to the job whose range holds it.
+__global__ void __launch_bounds__(256) k_split_batch(SplitBatch b) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= b.first[b.count]) return;
+  int q = 0;
+  while (i >= b.first[q + 1]) ++q;
+  split_b_one(b.B[q], b.ldb[q], b.tb[q] != 0, b.k[q], b.n[q], b.nj[q], i - b.first[q], b.out[q]);
 }
 
 // Split 8 fp32 (two float4) into the three bf16x8 fragment parts.
@@ -385,16 +411,18 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
   r.p = p;
   r.nj = (int)ceil_div(p.n, 32);
   r.nslab = ceil_div(p.k, kSlab);
-  r.bp = static_cast<const __bf16*>(ws);
+  r.bp = p.bsplit ? static_cast<const __bf16*>(p.bsplit) : static_cast<const __bf16*>(ws);
   r.c_vec = p.ldc % 4 == 0 && aligned16(p.C);
   const int64_t nparts = colsum_parts(p);
   r.part = nparts ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                              round_up((int64_t)sizeof(__bf16) * split_b_elems(p), 256))
                   : nullptr;
-  const int64_t threads = r.nslab * 2 * r.nj * 64;
-  hipLaunchKernelGGL(k_split_b, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, s, r, threads,
-                     static_cast<__bf16*>(ws));
-  GCN_TRY(check_launch("gemm weight split"));
+  if (!p.bsplit) {
+    const int64_t threads = split_threads(p.k, p.n);
+    hipLaunchKernelGGL(k_split_b, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, s, r, threads,
+                       static_cast<__bf16*>(ws));
+    GCN_TRY(check_launch("gemm weight split"));
+  }
   switch (r.nj) {
     case 1: launch_nj<1, 3>(r, s); break;
     case 2: launch_nj<2, 3>(r, s); break;
@@ -410,6 +438,35 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
   // the partial rows are a small matrix: its column sums by the two-level fixed-order pass
   void* cws = reinterpret_cast<char*>(r.part) + round_up((int64_t)sizeof(float) * nparts * p.n, 256);
   return launch_colsum(nparts, (int32_t)p.n, r.part, p.n, p.colsum, nullptr, nullptr, cws, s);
+}
+
+size_t gemm_rows_split_bytes(const SplitJob& j) {
+  return (size_t)round_up((int64_t)sizeof(__bf16) * ceil_div(j.k, kSlab) * 2 * ceil_div(j.n, 32) * 3 * kBlockBf16,
+                          256);
+}
+
+gcn_status launch_split_batch(const SplitJob* jobs, int count, hipStream_t s) {
+  if (count <= 0) return GCN_OK;
+  if (count > kMaxSplitJobs) return fail(GCN_E_UNSUPPORTED, "weight split: too many jobs");
+  SplitBatch b{};
+  b.count = count;
+  b.first[0] = 0;
+  for (int q = 0; q < count; ++q) {
+    const SplitJob& j = jobs[q];
+    if (j.k <= 0 || j.n <= 0 || j.n > kMaxN || !j.B || !j.out || !aligned16(j.out))
+      return fail(GCN_E_INVALID, "weight split: bad job");
+    b.B[q] = j.B;
+    b.out[q] = static_cast<__bf16*>(j.out);
+    b.ldb[q] = j.ldb;
+    b.k[q] = j.k;
+    b.n[q] = j.n;
+    b.tb[q] = j.tb ? 1 : 0;
+    b.nj[q] = (int32_t)ceil_div(j.n, 32);
+    b.first[q + 1] = b.first[q] + split_threads(j.k, j.n);
+  }
+  ProfScope prof("weight_split", 0, 0, 0, s);
+  hipLaunchKernelGGL(k_split_batch, dim3((unsigned)ceil_div(b.first[count], 256)), dim3(256), 0, s, b);
+  return check_launch("weight split batch");
 }
 
 }  // namespace gcn

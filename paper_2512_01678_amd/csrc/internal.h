@@ -166,6 +166,9 @@ struct GemmParams {
   // Row-panel product with GEMM_MASK only: also write the column sums of C (n floats,
   // fixed order) -- the bias gradient of the layer below, whose gradient C is.
   float* colsum = nullptr;
+  // Row-panel product: B already split into its bf16 planes (launch_split_batch); the
+  // product then skips its own split.
+  const void* bsplit = nullptr;
 };
 // Workspace of launch_gemm: split-k partials (A^T B), or the split B of the row-panel
 // product (A B, A B^T with n <= 256); 0 when neither applies.
@@ -174,6 +177,29 @@ bool gemm_split_k(const GemmParams& p);
 bool gemm_rows_supported(const GemmParams& p);
 size_t gemm_rows_workspace(const GemmParams& p);
 gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s);
+// Weights split once for several row-panel products (gcn_epoch: the weights do not change
+// between the forward and the backward pass).  A job is identified by the operand B as a
+// product sees it: pointer, pitch, transposition and the k x n shape.
+struct SplitJob {
+  const float* B;
+  int64_t ldb;
+  bool tb;
+  int64_t k, n;
+  void* out;  // gemm_rows_split_bytes(job) bytes, 16-byte aligned
+};
+constexpr int kMaxSplitJobs = 16;
+size_t gemm_rows_split_bytes(const SplitJob& j);
+gcn_status launch_split_batch(const SplitJob* jobs, int count, hipStream_t s);
+// The prepared planes for p's B, if any job matches it and p takes the row-panel kernel.
+inline GemmParams with_split(GemmParams p, const SplitJob* jobs, int count) {
+  if (!jobs || !gemm_rows_supported(p)) return p;
+  for (int i = 0; i < count; ++i)
+    if (jobs[i].B == p.B && jobs[i].ldb == p.ldb && jobs[i].tb == p.tb && jobs[i].k == p.k && jobs[i].n == p.n) {
+      p.bsplit = jobs[i].out;
+      break;
+    }
+  return p;
+}
 // Arithmetic of the dense products: bf16x6 (default) unless GCN_GEMM_MODE=fp32.
 bool gemm_bf16x6_mode();
 gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s);
