@@ -4,6 +4,7 @@
 // with the same code for the size query and the real call, and enqueues
 // kernels from the other translation units.  Nothing here allocates device
 // memory.
+#include <cstring>
 #include <string>
 
 #include "internal.h"
@@ -598,10 +599,15 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
   // Every weight in the two forms the row-panel products take it in (W for H W, W^T for
   // the input gradient), split once at the start: the weights change only in the Adam
   // step at the end.  A product that does not take the row-panel kernel ignores its job.
+  // GCN_EPOCH_PREP=0 turns both epoch-level shortcuts off (this split and the bias
+  // gradient of the loss pass): the products then split their own weights and the
+  // backward pass sums G itself, with bitwise the same results.
+  const char* prep_env = getenv("GCN_EPOCH_PREP");
+  const bool prep = !(prep_env && strcmp(prep_env, "0") == 0);
   SplitJob jobs[kMaxSplitJobs];
   int njobs = 0;
   int64_t job_at[kMaxSplitJobs];
-  for (int l = 0; l < L; ++l) {
+  for (int l = 0; l < L && prep; ++l) {
     const int64_t fi = m->layers[l].f_in, fo = m->layers[l].f_out;
     const float* const aligned_probe = reinterpret_cast<const float*>((uintptr_t)256);
     for (int form = 0; form < 2; ++form) {
@@ -630,14 +636,14 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
     const gcn_layer* ly = &m->layers[l];
     GCN_TRY(layer_fwd(g, ly, l == 0 ? d_X : m->act[l - 1], l == 0 ? x : nullptr, m->W[l], m->b[l],
                       l < L - 1 ? m->act[l] : m->grad[l], m->saved ? m->saved[l] : nullptr, d_labels,
-                      d_loss, nullptr, a, stream, bits_of(l), nullptr, l == L - 1 ? m->db[l] : nullptr, jobs,
-                      njobs));
+                      d_loss, nullptr, a, stream, bits_of(l), nullptr, prep && l == L - 1 ? m->db[l] : nullptr,
+                      jobs, njobs));
   }
   // with the bitmask, layer l's input-gradient product also sums the columns of G_{l-1}
   // (db of layer l - 1), which then skips its own column-sum pass over G_{l-1}; the last
   // layer's bias gradient comes out of the loss pass of the forward
   bool db_from_above[8] = {};
-  db_from_above[L - 1] = true;
+  db_from_above[L - 1] = prep;
   for (int l = L - 1; l >= 0; --l) {
     Arena a;
     a.base = base + bits_bytes;

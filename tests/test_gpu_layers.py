@@ -393,6 +393,27 @@ def test_epoch_bitwise_deterministic(G, small):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("rows", ["auto", "1"])
+def test_epoch_prep_is_exact(G, small, rows, monkeypatch):
+    """The epoch's weight split at its start (one launch for every row-panel product) and
+    the last bias gradient taken from the loss pass are rearrangements of the same
+    arithmetic: parameters, Adam moments and loss stay bitwise equal with them switched off
+    (rows=1 makes the products take the row-panel kernel at this size)."""
+    if rows != "auto":
+        monkeypatch.setenv("GCN_GEMM_ROWS", rows)
+    p = small
+    outs = []
+    for prep in ("1", "0"):
+        monkeypatch.setenv("GCN_EPOCH_PREP", prep)
+        m = G.Model(p.wl.n, p.wl.widths, p.Ws, p.bs)
+        for _ in range(3):
+            m.epoch(p.dg, X=dev(p.X), labels=dev(p.y))
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in m.W + m.b + m.mW + m.vW + m.mb + m.vb + m.dW + m.db + [m.loss]])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 # ---------------------------------------------------------------------------
 # full-size workload in the benchmark's launch configuration: sampled rows
 # ---------------------------------------------------------------------------
