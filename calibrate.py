@@ -6,7 +6,7 @@ support of density p, as in the RMAT workload) is drawn on the device and both
 products of layer 0 are timed both ways:
 
   forward   X W    (F x F1):  dense MFMA GEMM      vs  X_csr SpMM
-  backward  X^T Q  (N x F1):  dense MFMA GEMM (TN) vs  X_csc SpMM
+  backward  X^T Q  (N x F1):  dense MFMA GEMM (TN) vs  X_csc SpMM (gcn_spmm_xt)
 
 Efficiencies count useful work only: eta_dense = 2 N F F1 / t_dense and
 eta_sparse = 2 nnz F1 / t_sparse, so gamma = eta_sparse / eta_dense and the sparse
@@ -80,9 +80,9 @@ def main():
             dense_f = timed(lambda: G.gemm(G.OP_NN, X, W, out, ws=ws), args.reps)
             dense_b = timed(lambda: G.gemm(G.OP_TN, X, Q, dW, ws=ws), args.reps)
             sparse_f = timed(lambda: G.spmm(sx.row_ptr, sx.col[:nnz], sx.val[:nnz], W, out), args.reps)
-            split = sx.c.csc_split  # the plan gcn_feature_stats filled in
-            sparse_b = timed(lambda: G.spmm(sx.col_ptr, sx.row[:nnz], sx.cval[:nnz], Q, dW, split=split),
-                             args.reps)
+            # the backward product in the form layer 0's backward takes (tiled by row chunks
+            # where the columns are long enough)
+            sparse_b = timed(lambda: G.spmm_xt(sx, Q, dW), args.reps)
             dflop, sflop = 2.0 * n * F * f1, 2.0 * nnz * f1
             r = {"F": F, "density": nnz / (n * F), "nnz": nnz,
                  "dense_fwd_ms": round(dense_f, 3), "sparse_fwd_ms": round(sparse_f, 3),

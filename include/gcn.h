@@ -367,6 +367,23 @@ gcn_status gcn_spmm(int64_t nrows, int64_t nnz, const int64_t* d_ptr, const int3
                     hipStream_t stream);
 
 /*
+ * gcn_spmm_xt -- C = X^T B with X (n x f) in its CSC view: the backward SpMM over
+ * X_csc of Algorithm 1 (dW_0 = X^T Q of a sparse first layer).  Asynchronous.
+ * d_col_ptr: f + 1 int64; d_row, d_cval: nnz row indices (ascending within a column,
+ * 0 <= row < n) and values, as gcn_feature_stats writes them; d_B: n x w (pitch ldb);
+ * d_C: f x w (pitch ldc), overwritten.  csc_split: plan of the long columns (or NULL).
+ * When the columns hold at least 16 entries per 8,192-row chunk on average and n spans
+ * four chunks or more, the rows are cut into such chunks: every (column, chunk) range
+ * is summed into a partial in the workspace (the chunk's rows of B stay in one L2) and
+ * the partials are added in chunk order; otherwise each column is one gathered sum.
+ * GCN_XT=plain / =tiled forces either form.  Deterministic; w <= 256 for the chunked
+ * form.  Workspace: query with d_ws == NULL.
+ */
+gcn_status gcn_spmm_xt(int32_t n, int32_t f, int64_t nnz, const int64_t* d_col_ptr, const int32_t* d_row,
+                       const float* d_cval, const gcn_split* csc_split, const float* d_B, int64_t ldb,
+                       int32_t w, float* d_C, int64_t ldc, void* d_ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
  * gcn_column_sums -- out[c] = sum_i G[i,c] (the bias gradient) and, when
  * d_row_vals != NULL, *d_mean = (1/rows) sum_i row_vals[i].  Fixed summation
  * order.  Asynchronous.

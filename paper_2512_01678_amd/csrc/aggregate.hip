@@ -28,6 +28,7 @@
 // and applies the same epilogue.
 #include "agg_device.h"
 
+#include <cstring>
 #include <type_traits>
 
 namespace gcn {
@@ -358,6 +359,161 @@ __global__ void k_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col) {
   if (i < n) col[i] = (int32_t)i;
 }
 }  // namespace
+
+namespace {
+// X^T Q from the CSC view, tiled by row chunks.  Column j of X_csc lists its nonzeros
+// (i, x) with i ascending; sum_i x Q[i, :] gathers a row of Q per nonzero, and Q (n rows)
+// is far larger than an L2.  Cut the rows into chunks of kXtChunk rows (the chunk's rows
+// of Q, at most 8192 x 128 floats = 4 MB, fit one XCD's L2), sum each (column, chunk)
+// range into a partial, and give every workgroup of one chunk the same XCD: workgroup
+// ids are dealt to the XCDs in turn, so id % 8 names the XCD, and XCD x takes chunks x,
+// x + 8, ... one after the other, all columns of a chunk before the next.  The partials
+// are added in chunk order afterwards (the same fixed order every run).
+constexpr int64_t kXtChunk = 8192;
+constexpr int kXcds = 8;
+
+// off[c * F + j] = first entry of column j whose row is >= c * kXtChunk (c = 0..nchunk).
+__global__ void __launch_bounds__(256) k_xt_offsets(int32_t F, const int64_t* col_ptr, const int32_t* row,
+                                                    int64_t nchunk, int64_t* off) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (nchunk + 1) * F) return;
+  const int64_t c = t / F;
+  const int32_t j = (int32_t)(t % F);
+  int64_t lo = col_ptr[j], hi = col_ptr[j + 1];
+  const int64_t r0 = c * kXtChunk;
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    if (row[mid] < r0) lo = mid + 1;
+    else hi = mid;
+  }
+  off[t] = lo;
+}
+
+// part[c][j][0 .. w) = sum over column j's entries in chunk c of x Q[i, :].
+template <int LANES, int VEC>
+__global__ void __launch_bounds__(kBlock) k_xt_tiled(AggParams p, const int64_t* off, int64_t nchunk,
+                                                     int64_t groups, int slots, float* part) {
+  const Lanes L = lanes_of<LANES, VEC>(slots);
+  const int64_t id = blockIdx.x;
+  const int64_t k = id / kXcds;
+  const int64_t c = (k / groups) * kXcds + id % kXcds;
+  if (c >= nchunk) return;
+  const int64_t j = (k % groups) * (kBlock / L.gw) + threadIdx.x / L.gw;
+  if (j >= p.n) return;  // whole groups leave together
+  const int64_t beg = off[c * p.n + j], end = off[(c + 1) * p.n + j];
+  const bool cok = L.c0 < p.w;
+  const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
+  if (!cok || L.slot != 0) return;
+  float* out = part + (c * p.n + j) * p.w + L.c0;
+  if (VEC == 4 && p.w % 4 == 0 && L.c0 + 4 <= p.w) {
+    Vec<VEC>::store(out, acc);
+  } else {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i)
+      if (L.c0 + i < p.w) out[i] = Vec<VEC>::get(acc, i);
+  }
+}
+}  // namespace
+
+int64_t xt_chunk_rows() { return kXtChunk; }
+
+// GCN_XT=plain keeps the untiled CSC product, =tiled takes the tiled one at any size;
+// unset: tiled from four chunks of rows on when a column has at least 16 entries per
+// chunk on average.  Measured on the RMAT features (2,097,152 x 4096, w = 128): 1 %
+// density 5.87 -> 2.42 ms, 10 % 41.6 -> 19.2 ms, but 0.1 % (about 8 entries per column
+// and chunk) 0.62 -> 0.74 ms, where the partials cost more than the gathers save.
+bool xt_tiled_enabled(int64_t n, int32_t F, int64_t nnz, int32_t w) {
+  if (w <= 0 || w > 256 || F <= 0) return false;
+  const char* e = getenv("GCN_XT");
+  if (e && strcmp(e, "plain") == 0) return false;
+  if (e && strcmp(e, "tiled") == 0) return true;
+  const int64_t nchunk = ceil_div(n, kXtChunk);
+  return nchunk >= 4 && nnz >= 16 * (int64_t)F * nchunk;
+}
+
+size_t xt_tiled_workspace(int64_t n, int32_t F, int32_t w) {
+  const int64_t nchunk = std::max<int64_t>(1, ceil_div(n, kXtChunk));
+  return (size_t)round_up(8 * (nchunk + 1) * (int64_t)F, 256) + (size_t)round_up(4 * nchunk * (int64_t)F * w, 256);
+}
+
+gcn_status launch_spmm_xt_tiled(int64_t n, int32_t F, const int64_t* col_ptr, const int32_t* row, const float* cval,
+                                int64_t nnz, const float* B, int64_t ldb, int32_t w, float* C, int64_t ldc, void* ws,
+                                hipStream_t s) {
+  if (F == 0 || w == 0) return GCN_OK;
+  if (w > 256) return fail(GCN_E_UNSUPPORTED, "tiled transpose product: width above 256");
+  if (!ws) return fail(GCN_E_INVALID, "tiled transpose product needs a workspace");
+  const int64_t nchunk = std::max<int64_t>(1, ceil_div(n, kXtChunk));
+  int64_t* off = static_cast<int64_t*>(ws);
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + round_up(8 * (nchunk + 1) * (int64_t)F, 256));
+  char name[64];
+  snprintf(name, sizeof name, "spmm_xtq_tiled_w%d", w);
+  ProfScope prof(name, w, F, nnz, s);
+  hipLaunchKernelGGL(k_xt_offsets, dim3((unsigned)ceil_div((nchunk + 1) * F, 256)), dim3(256), 0, s, F, col_ptr, row,
+                     nchunk, off);
+  GCN_TRY(check_launch("tiled transpose offsets"));
+  AggParams p{};
+  p.n = F;
+  p.row_ptr = col_ptr;
+  p.col = row;
+  p.val = cval;
+  p.kind = AGG_W_VAL;
+  p.M = B;
+  p.ldm = ldb;
+  p.w = w;
+  const bool vec4 = ldb % 4 == 0 && aligned16(B);
+  int lanes = 1;
+  while (lanes < ceil_div(w, vec4 ? 4 : 1) && lanes < 64) lanes <<= 1;
+  if (!vec4 && w > 64) return fail(GCN_E_UNSUPPORTED, "tiled transpose product: rows of Q must be 16-byte aligned above width 64");
+  const int64_t per_col = std::max<int64_t>(1, nnz / std::max<int64_t>(1, (int64_t)F * nchunk));
+  const int slots = pick_slots(lanes, per_col * F, F);
+  const int gw = lanes * slots;
+  const int64_t groups = ceil_div(F, kBlock / gw);
+  const int64_t grid = ceil_div(nchunk, kXcds) * kXcds * groups;
+  if (grid > INT32_MAX) return fail(GCN_E_RANGE, "tiled transpose product: too many workgroups");
+  auto run = [&](auto ln, auto vc) {
+    constexpr int LN = decltype(ln)::value, VC = decltype(vc)::value;
+    hipLaunchKernelGGL((k_xt_tiled<LN, VC>), dim3((unsigned)grid), dim3(kBlock), 0, s, p, off, nchunk, groups, slots,
+                       part);
+  };
+  using I = std::integral_constant<int, 4>;
+  using O = std::integral_constant<int, 1>;
+  switch (lanes) {
+    case 1: vec4 ? run(std::integral_constant<int, 1>{}, I{}) : run(std::integral_constant<int, 1>{}, O{}); break;
+    case 2: vec4 ? run(std::integral_constant<int, 2>{}, I{}) : run(std::integral_constant<int, 2>{}, O{}); break;
+    case 4: vec4 ? run(std::integral_constant<int, 4>{}, I{}) : run(std::integral_constant<int, 4>{}, O{}); break;
+    case 8: vec4 ? run(std::integral_constant<int, 8>{}, I{}) : run(std::integral_constant<int, 8>{}, O{}); break;
+    case 16: vec4 ? run(std::integral_constant<int, 16>{}, I{}) : run(std::integral_constant<int, 16>{}, O{}); break;
+    case 32: vec4 ? run(std::integral_constant<int, 32>{}, I{}) : run(std::integral_constant<int, 32>{}, O{}); break;
+    default: vec4 ? run(std::integral_constant<int, 64>{}, I{}) : run(std::integral_constant<int, 64>{}, O{}); break;
+  }
+  GCN_TRY(check_launch("tiled transpose product"));
+  return launch_partial_sum(part, nchunk, F, w, C, ldc, s);
+}
+
+size_t spmm_xt_workspace(int64_t n, int32_t F, int64_t nnz, int32_t w, const gcn_split* csc_split) {
+  if (xt_tiled_enabled(n, F, nnz, w)) return xt_tiled_workspace(n, F, w);
+  return aggregate_workspace(csc_split, w);
+}
+
+gcn_status launch_spmm_xt(int64_t n, int32_t F, int64_t nnz, const int64_t* col_ptr, const int32_t* row,
+                          const float* cval, const gcn_split* csc_split, const float* B, int64_t ldb, int32_t w,
+                          float* C, int64_t ldc, void* ws, hipStream_t s) {
+  if (xt_tiled_enabled(n, F, nnz, w))
+    return launch_spmm_xt_tiled(n, F, col_ptr, row, cval, nnz, B, ldb, w, C, ldc, ws, s);
+  AggParams p{};
+  p.n = F;
+  p.row_ptr = col_ptr;
+  p.col = row;
+  p.val = cval;
+  p.M = B;
+  p.ldm = ldb;
+  p.w = w;
+  p.Z = C;
+  p.ldz = ldc;
+  p.epi = AGG_NONE;
+  p.tag = "spmm_xtq";
+  return launch_aggregate(p, nnz, csc_split, ws, s);
+}
 
 gcn_status launch_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx, const float* val,
                                 const float* B, int64_t ldb, int32_t w, int64_t out_rows, float* C, int64_t ldc,

@@ -352,7 +352,8 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
   GemmParams dw = gemm(L->f_in, L->f_out, n, Hin, L->ld_in, true, Q, ldq, false, dW, L->f_out);
   void* gws = x ? nullptr : a.take<char>((int64_t)gemm_workspace(dw));
   const size_t agg_need = std::max(aggregate_workspace(&g->split, L->f_out),
-                                   x && x->col_ptr ? aggregate_workspace(&x->csc_split, L->f_out) : (size_t)0);
+                                   x && x->col_ptr ? spmm_xt_workspace(n, x->f, x->nnz, L->f_out, &x->csc_split)
+                                                   : (size_t)0);
   void* aws = a.take<char>((int64_t)agg_need);
   GemmParams t = gemm(n, L->f_in, L->f_out, Q, ldq, false, W, L->f_out, true, Gprev, L->ld_in);
   t.epi = GEMM_MASK;
@@ -379,19 +380,9 @@ gcn_status layer_bwd(const gcn_graph* g, const gcn_layer* L, const float* G, con
     // no CSC view: dW = X^T Q by atomic adds from the CSR rows (Section IV-D)
     GCN_TRY(launch_spmm_t_atomic(n, x->row_ptr, x->col, x->val, Q, ldq, L->f_out, x->f, dW, L->f_out, x->nnz, s));
   } else if (x) {
-    AggParams p{};
-    p.n = x->f;
-    p.row_ptr = x->col_ptr;
-    p.col = x->row;
-    p.val = x->cval;
-    p.M = Q;
-    p.ldm = ldq;
-    p.w = L->f_out;
-    p.Z = dW;
-    p.ldz = L->f_out;
-    p.epi = AGG_NONE;
-    p.tag = "spmm_xtq";
-    GCN_TRY(launch_aggregate(p, x->nnz, &x->csc_split, aws, s));
+    // dW = X^T Q from the CSC view (tiled by row chunks where that pays)
+    GCN_TRY(launch_spmm_xt(n, x->f, x->nnz, x->col_ptr, x->row, x->cval, &x->csc_split, Q, ldq, L->f_out, dW,
+                           L->f_out, aws, s));
   } else {
     GCN_TRY(launch_gemm(dw, gws, s));
   }
@@ -770,6 +761,23 @@ gcn_status gcn_spmm(int64_t nrows, int64_t nnz, const int64_t* d_ptr, const int3
   p.epi = AGG_NONE;
   p.tag = "spmm";
   return launch_aggregate(p, nnz, split, d_ws, stream);
+}
+
+gcn_status gcn_spmm_xt(int32_t n, int32_t f, int64_t nnz, const int64_t* d_col_ptr, const int32_t* d_row,
+                       const float* d_cval, const gcn_split* csc_split, const float* d_B, int64_t ldb,
+                       int32_t w, float* d_C, int64_t ldc, void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (n < 0 || f < 0 || nnz < 0 || w < 0 || ldb < w || ldc < w) return fail(GCN_E_INVALID, "gcn_spmm_xt: bad size or pitch");
+  if (csc_split && csc_split->rows && csc_split->n_long > 0 && (!csc_split->first || !csc_split->owner))
+    return fail(GCN_E_INVALID, "gcn_spmm_xt: split plan arrays missing");
+  if (w > 256 && xt_tiled_enabled(n, f, nnz, w)) return fail(GCN_E_UNSUPPORTED, "gcn_spmm_xt: width above 256");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, spmm_xt_workspace(n, f, nnz, w, csc_split), "gcn_spmm_xt", &query));
+  if (query) return GCN_OK;
+  if (f > 0 && w > 0 && (!d_col_ptr || (nnz > 0 && (!d_row || !d_cval || !d_B)) || !d_C))
+    return fail(GCN_E_INVALID, "gcn_spmm_xt: NULL argument");
+  if (f == 0 || w == 0) return GCN_OK;
+  return launch_spmm_xt(n, f, nnz, d_col_ptr, d_row, d_cval, csc_split, d_B, ldb, w, d_C, ldc, d_ws, stream);
 }
 
 gcn_status gcn_column_sums(int64_t rows, int32_t w, const float* d_G, int64_t ldg, float* d_out,

@@ -459,6 +459,18 @@ __global__ void __launch_bounds__(256) k_splitk_reduce(const float* part, int64_
   }
 }
 
+}  // namespace
+
+gcn_status launch_partial_sum(const float* part, int64_t splits, int64_t m, int64_t n, float* C, int64_t ldc,
+                              hipStream_t s) {
+  const int64_t total = m * n;
+  if (total == 0) return GCN_OK;
+  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, part, splits, m, n, C,
+                     ldc, nullptr);
+  return check_launch("partial sum");
+}
+
+namespace {
 struct Shape {
   int bm, bn;
 };

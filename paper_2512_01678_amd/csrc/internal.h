@@ -122,6 +122,24 @@ gcn_status launch_aggregate_max_bwd(const AggParams& p, int64_t nnz, const int32
 gcn_status launch_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx, const float* val,
                                 const float* B, int64_t ldb, int32_t w, int64_t out_rows, float* C, int64_t ldc,
                                 int64_t nnz, hipStream_t s);
+// C (F x w) = X^T B from X's CSC view (col_ptr over F columns, ascending row indices
+// in row / values in cval), in row chunks of xt_chunk_rows() rows: each (column, chunk)
+// sum goes to a partial, and the partials are added in chunk order.  Deterministic.
+// w <= 256.
+int64_t xt_chunk_rows();
+bool xt_tiled_enabled(int64_t n, int32_t F, int64_t nnz, int32_t w);
+size_t xt_tiled_workspace(int64_t n, int32_t F, int32_t w);
+gcn_status launch_spmm_xt_tiled(int64_t n, int32_t F, const int64_t* col_ptr, const int32_t* row, const float* cval,
+                                int64_t nnz, const float* B, int64_t ldb, int32_t w, float* C, int64_t ldc, void* ws,
+                                hipStream_t s);
+// X^T B from the CSC view in the form xt_tiled_enabled picks (gcn_spmm_xt).
+size_t spmm_xt_workspace(int64_t n, int32_t F, int64_t nnz, int32_t w, const gcn_split* csc_split);
+gcn_status launch_spmm_xt(int64_t n, int32_t F, int64_t nnz, const int64_t* col_ptr, const int32_t* row,
+                          const float* cval, const gcn_split* csc_split, const float* B, int64_t ldb, int32_t w,
+                          float* C, int64_t ldc, void* ws, hipStream_t s);
+// C (m x n, pitch ldc) = sum over z < splits of part[z] (m x n, dense), in order of z.
+gcn_status launch_partial_sum(const float* part, int64_t splits, int64_t m, int64_t n, float* C, int64_t ldc,
+                              hipStream_t s);
 // Identity operator in CSR form: row_ptr[i] = i, col[i] = i.
 gcn_status launch_identity_csr(int32_t n, int64_t* row_ptr, int32_t* col, hipStream_t s);
 // Only the long rows of a split plan (chunk sums, then their combination), no epilogue.

@@ -103,6 +103,7 @@ _SIG = {
                                     P]),
     "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
     "gcn_spmm": (i32, [i64, i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
+    "gcn_spmm_xt": (i32, [i32, i32, i64, P, P, P, C.POINTER(gcn_split), P, i64, i32, P, i64, P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
     "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
     "gcn_adam_device_step": (i32, [C.POINTER(gcn_adam_tensor), i32, P, f64, f64, f64, f64, P]),
@@ -318,6 +319,15 @@ def spmm(ptr, idx, val, B, out, split: gcn_split | None = None, stream=None):
     _run_ws(_lib.gcn_spmm, (nrows, idx.numel(), _ptr(ptr), _ptr(idx), _ptr(val), B.shape[0], B.shape[1], _ptr(B),
                             _ld(B), _ptr(out), _ld(out), C.byref(split) if split is not None else None),
             (P(_stream(stream)),), "gcn_spmm", None, out.device)
+    return out
+
+
+def spmm_xt(sx: "SparseFeatures", B: torch.Tensor, out: torch.Tensor, stream=None):
+    """out (f x w) = X^T B from the CSC view of sparse features sx (Algorithm 1, Backward)."""
+    n, w = B.shape
+    c = sx.c
+    _run_ws(_lib.gcn_spmm_xt, (c.n, c.f, c.nnz, c.col_ptr, c.row, c.cval, C.byref(c.csc_split), _ptr(B), _ld(B), w,
+                               _ptr(out), _ld(out)), (P(_stream(stream)),), "gcn_spmm_xt", None, out.device)
     return out
 
 

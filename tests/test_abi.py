@@ -118,6 +118,12 @@ def test_host_validation_rejects_bad_calls(G):
     assert L.gcn_aggregate(C.byref(bad), 0, 40, 1, 40, None, 0, None, 0, 1, 40, None, C.byref(nb), None) == G.E_INVALID
     # spmm: bad pitch
     assert L.gcn_spmm(10, 20, 1, 1, 1, 5, 8, 1, 7, 1, 8, None, None, C.byref(nb), None) == G.E_INVALID
+    # spmm_xt: bad pitch, negative sizes; size query of the chunked form (n = 4 chunks of
+    # 8192 rows, 16 entries per column and chunk): offsets (5 x 3 int64) + partials (4 x 3 x 8)
+    assert L.gcn_spmm_xt(10, 3, 5, 1, 1, 1, None, 1, 7, 8, 1, 8, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_spmm_xt(-1, 3, 5, 1, 1, 1, None, 1, 8, 8, 1, 8, None, C.byref(nb), None) == G.E_INVALID
+    assert L.gcn_spmm_xt(4 * 8192, 3, 16 * 3 * 4, 1, 1, 1, None, 1, 8, 8, 1, 8, None, C.byref(nb), None) == G.OK
+    assert nb.value == 256 + 512
     # adam: step 0, too many tensors
     assert L.gcn_adam(None, 0, 0, 0.01, 0.9, 0.999, 1e-8, None) == G.E_INVALID
     arr = (G.gcn_adam_tensor * 17)()

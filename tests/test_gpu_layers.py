@@ -162,7 +162,10 @@ def test_layer_backward(G, orc, small, order, fi, fo, first):
         assert_mag_close(host(Gprev), ref, mag, f"G_prev {order}")
 
 
-def test_layer_sparse_input(G, orc, cora):
+@pytest.mark.parametrize("xt", ["plain", "tiled"])
+def test_layer_sparse_input(G, orc, cora, xt, monkeypatch):
+    """xt: the CSC product for dW = X^T Q untiled, or tiled by row chunks (one chunk here)."""
+    monkeypatch.setenv("GCN_XT", xt)
     og, dg, n = cora.og, cora.dg, cora.wl.n
     X, W0, b0 = cora.X, cora.Ws[0], cora.bs[0] + 0.05
     info, sx = G.feature_stats(dev(X))
@@ -180,6 +183,41 @@ def test_layer_sparse_input(G, orc, cora):
     Q = orc.aggregate(og, Gr)
     assert_mag_close(host(dW), orc.matmul(X.T, Q), orc.matmul(np.abs(X).T, abs_agg(orc, og, Gr)),
                      "sparse layer-0 dW")
+
+
+@pytest.mark.parametrize("w", [40, 37, 128])
+def test_sparse_weight_gradient_row_chunks(G, orc, w, monkeypatch):
+    """dW = X^T Q from the CSC view tiled by row chunks: three full chunks of rows and a
+    ragged fourth, an empty feature column, a column with a nonzero in every row, widths
+    with and without 16-byte partial rows; against the fp64 product and the untiled form.
+    The graph has no edges, so Q = G."""
+    n, F = 3 * 8192 + 1234, 700  # the library tiles rows in chunks of 8192
+    rng = np.random.default_rng(21)
+    X = np.where(rng.random((n, F)) < 0.02, rng.standard_normal((n, F)), 0.0).astype(np.float32)
+    X[:, 5] = 0.0
+    X[:, 9] = rng.standard_normal(n).astype(np.float32)
+    dg = G.build_csr(n, dev(np.zeros(0, np.int32)), dev(np.zeros(0, np.int32)))
+    info, sx = G.feature_stats(dev(X))
+    assert info["mode"] == G.SPARSE
+    L = G.make_layer(F, w, F, G.pitch(w), G.ACT_RELU, 0)
+    Gr = (rng.standard_normal((n, w)) / n).astype(np.float32)
+    W0 = rng.standard_normal((F, w)).astype(np.float32)
+    out = {}
+    for xt in ("plain", "tiled"):
+        monkeypatch.setenv("GCN_XT", xt)
+        dW = torch.zeros((F, w), device="cuda")
+        db = torch.zeros(w, device="cuda")
+        G.layer_bwd(dg, L, pad(G, Gr), None, sx, None, dev(W0), dW, db, None)
+        out[xt] = host(dW)
+        # the same product through its own entry point
+        C2 = torch.full((F, w), float("nan"), device="cuda")
+        G.spmm_xt(sx, dev(Gr), C2)
+        out[xt + " (gcn_spmm_xt)"] = host(C2)
+    ref = orc.matmul(X.T, Gr)
+    mag = orc.matmul(np.abs(X).T, np.abs(Gr))
+    for xt, got in out.items():
+        assert_mag_close(got, ref, mag, f"X^T Q ({xt})")
+    assert np.all(out["tiled"][5] == 0.0)
 
 
 # ---------------------------------------------------------------------------
@@ -455,9 +493,12 @@ def test_arxiv_like_full_size_sampled(G, orc):
             assert_mag_close(host(m.grad[l - 1])[rows], ref, mag, f"full-size G_{l - 1} rows")
 
 
-def test_epoch_rmat_4096_features_sparse(G, orc):
+@pytest.mark.parametrize("xt", ["plain", "tiled"])
+def test_epoch_rmat_4096_features_sparse(G, orc, xt, monkeypatch):
     """RMAT graph with 4096-wide nonnegative features at 10 % density (the RMAT workload's
-    recipe on 2^14 nodes): sparse path chosen by the probe, one epoch against the oracle."""
+    recipe on 2^14 nodes): sparse path chosen by the probe, one epoch against the oracle;
+    xt: the untiled or the row-chunk-tiled CSC product for dW_0 (two chunks here)."""
+    monkeypatch.setenv("GCN_XT", xt)
     from gcn_synth import device
     wl = gs.Workload("rmat14_p0.1", 1 << 14, "rmat", 1 << 18, (4096, 128, 32), "nonneg", 0.1, rmat_scale=14)
     s, d = gs.rmat(14, 1 << 18)
