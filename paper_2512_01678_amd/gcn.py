@@ -133,9 +133,15 @@ def _stream(stream=None):
     return s.cuda_stream
 
 
+def _sectors(w: int, p: int) -> float:
+    return sum((((4 * p * r) % 64) + 4 * w + 63) // 64 for r in range(16)) / 16.0
+
+
 def pitch(w: int) -> int:
-    """Row pitch used for library-owned activations: width rounded up to 4 floats."""
-    return (w + 3) // 4 * 4
+    """Row pitch for activations and gradients (rows the aggregation gathers): w rounded up
+    to 4 floats, or to 16 where that makes a row touch fewer 64-byte sectors on average."""
+    a, b = (w + 3) // 4 * 4, (w + 15) // 16 * 16
+    return b if _sectors(w, b) < _sectors(w, a) else a
 
 
 def padded(rows: int, w: int, device="cuda", fill=None):
