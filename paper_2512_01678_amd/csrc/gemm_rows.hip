@@ -268,6 +268,31 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   // 169,343 x 256 x 256 product).
   float* stage = reinterpret_cast<float*>(lds) + wave * kRowsPerWave * kStagePitch;
   const int sr = l / 16, sc = 4 * (l % 16);  // read-back: rows sr + 4 i, columns sc .. sc + 3
+  // Every bias value and mask word the epilogue uses, requested before its first store:
+  // one counter tracks a wavefront's loads and stores alike, so a wait for a load issued
+  // between stores also waits for those stores, and loads inside the store loop would
+  // serialise it on store completion.
+  constexpr int kPairs = (NJ + 1) / 2;
+  float bias_all[kPairs][4];
+  uint32_t mask_all[kPairs][EPI == GEMM_MASK ? 8 : 1];
+#pragma unroll
+  for (int jp = 0; jp < kPairs; ++jp) {
+    const int64_t col = (int64_t)jp * 64 + sc;
+    const bool cin = col < p.n;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) bias_all[jp][q] = p.bias && cin && col + q < p.n ? p.bias[col + q] : 0.f;
+    if constexpr (EPI == GEMM_MASK) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int64_t row = row0 + sr + 4 * i;
+        mask_all[jp][i] = row < p.m && cin ? p.mask_bits[row * p.ld_mask_bits + col / 32] : 0u;
+      }
+    }
+  }
+  // Wait for them here, once: the compiler cannot prove them complete across the
+  // per-row branches below and would otherwise wait again (for every store so far) at
+  // each use.  s_waitcnt vmcnt(0), expcnt and lgkmcnt not waited for.
+  __builtin_amdgcn_s_waitcnt(0xF70);
 #pragma unroll
   for (int j0 = 0; j0 < NJ; j0 += 2) {
 #pragma unroll
@@ -279,10 +304,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int64_t col = (int64_t)j0 * 32 + sc;
     const bool cin = col < p.n, full = col + 4 <= p.n;
-    float bias[4] = {0.f, 0.f, 0.f, 0.f};
-    if (p.bias && cin)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) bias[q] = col + q < p.n ? p.bias[col + q] : 0.f;
+    const float* bias = bias_all[j0 / 2];
     // bitmask words: 8 lanes (32 columns) per word; the lanes of a word share the row
     const int64_t word = col / 32;
     const int shift = (int)(col % 32);
@@ -306,7 +328,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
         }
       }
       if constexpr (EPI == GEMM_MASK) {
-        const uint32_t mw = rin && cin ? p.mask_bits[row * p.ld_mask_bits + word] >> shift : 0u;
+        const uint32_t mw = mask_all[j0 / 2][i] >> shift;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           v[q] = (mw >> q) & 1u ? v[q] : 0.f;
