@@ -145,6 +145,10 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // wave-uniform: scalar registers
   const int h = l / 32, l32 = l % 32;
   const int64_t row0 = (int64_t)blockIdx.x * kRowsPerBlock + (int64_t)wave * kRowsPerWave;
+  // column group: tiles jb .. jb + NJ - 1 of the r.nj column tiles (one group unless the
+  // launch splits the columns over blockIdx.y)
+  const int jb = (int)blockIdx.y * NJ;
+  const int64_t cb = (int64_t)jb * 32;
   const int64_t nslab = r.nslab, nstep = 2 * nslab;
 
   // this lane's A row (rows past the end re-read the last row; never stored)
@@ -170,7 +174,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   };
   const u32x4* bsrc = reinterpret_cast<const u32x4*>(r.bp);
   auto load_b = [&](int64_t g, u32x4 (&rb)[kPer]) __attribute__((always_inline)) {
-    const u32x4* q = bsrc + g * kChunks;
+    const u32x4* q = bsrc + (g * r.nj + jb) * (3 * 64);
 #pragma unroll
     for (int i = 0; i < kPer; ++i)
       if (kChunks % kThreads == 0 || tid + i * kThreads < kChunks) rb[i] = q[tid + i * kThreads];
@@ -277,7 +281,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   uint32_t mask_all[kPairs][EPI == GEMM_MASK ? 8 : 1];
 #pragma unroll
   for (int jp = 0; jp < kPairs; ++jp) {
-    const int64_t col = (int64_t)jp * 64 + sc;
+    const int64_t col = cb + (int64_t)jp * 64 + sc;
     const bool cin = col < p.n;
 #pragma unroll
     for (int q = 0; q < 4; ++q) bias_all[jp][q] = p.bias && cin && col + q < p.n ? p.bias[col + q] : 0.f;
@@ -302,7 +306,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
     // the wavefront's own staging area: LDS accesses of one wavefront complete in order,
     // the fence keeps the compiler from reordering them
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    const int64_t col = (int64_t)j0 * 32 + sc;
+    const int64_t col = cb + (int64_t)j0 * 32 + sc;
     const bool cin = col < p.n, full = col + 4 <= p.n;
     const float* bias = bias_all[j0 / 2];
     // bitmask words: 8 lanes (32 columns) per word; the lanes of a word share the row
@@ -369,7 +373,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
       // the workgroup's partial row: the wavefronts' sums of column t, in wavefront order
       __syncthreads();
       const float* ws = reinterpret_cast<const float*>(lds) + kWaves * kRowsPerWave * kStagePitch;
-      for (int t = tid; t < p.n; t += kThreads) {
+      const int64_t ce = cb + NJ * 32 < p.n ? cb + NJ * 32 : p.n;
+      for (int64_t t = cb + tid; t < ce; t += kThreads) {
         float v = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) v += ws[w * kMaxN + t];
@@ -380,8 +385,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
 }
 
 template <int NJ, int PD>
-void launch_nj(const RowsArgs& r, hipStream_t s) {
-  const dim3 grid((unsigned)ceil_div(r.p.m, kRowsPerBlock));
+void launch_nj(const RowsArgs& r, hipStream_t s, unsigned groups = 1) {
+  const dim3 grid((unsigned)ceil_div(r.p.m, kRowsPerBlock), groups);
   switch (r.p.epi) {
     case GEMM_RELU: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_RELU>), grid, dim3(kThreads), 0, s, r); break;
     case GEMM_MASK: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_MASK>), grid, dim3(kThreads), 0, s, r); break;
@@ -445,7 +450,16 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
                        static_cast<__bf16*>(ws));
     GCN_TRY(check_launch("gemm weight split"));
   }
-  switch (r.nj) {
+  // With a short k the matrix work is small and the epilogue (every column of 32 rows per
+  // wavefront) dominates; with fewer than 2048 row panels (8 per CU) the last wave of
+  // workgroups also leaves CUs idle.  Then 8 column tiles go to two workgroups of 4 each
+  // (half the accumulators per wavefront, twice the workgroups), which read A twice.
+  // Measured on the width-40 input gradient: 169,343 rows 81.2 -> 72.3 us; at 2,449,029
+  // rows (19,133 panels) 0.80 -> 0.82 ms, so not there.  GCN_ROWS_GROUPS=1 keeps one group.
+  const char* ge = getenv("GCN_ROWS_GROUPS");
+  const bool grouped = r.nj == 8 && p.k <= 64 && ceil_div(p.m, kRowsPerBlock) < 2048 && !(ge && strcmp(ge, "1") == 0);
+  if (grouped) launch_nj<4, 2>(r, s, 2);
+  else switch (r.nj) {
     case 1: launch_nj<1, 3>(r, s); break;
     case 2: launch_nj<2, 3>(r, s); break;
     case 3: launch_nj<3, 2>(r, s); break;

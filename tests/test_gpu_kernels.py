@@ -328,6 +328,33 @@ def test_gemm_row_panels(G, op, shape, monkeypatch):
     assert_mag_close(host(C), ref * (mask > 0), mag, f"rows {op} mask")
 
 
+@pytest.mark.parametrize("op", ["NN", "NT"])
+@pytest.mark.parametrize("shape", [(600, 256, 33), (4099, 250, 40), (300, 226, 64)], ids=lambda s: "x".join(map(str, s)))
+def test_gemm_row_panels_column_groups(G, op, shape, monkeypatch):
+    """Short k: the 8 column tiles go to two workgroups of 4; every output element keeps
+    its summation order, so the result equals the one-group launch bit for bit."""
+    monkeypatch.setenv("GCN_GEMM_ROWS", "1")
+    m, n, k = shape
+    rng = np.random.default_rng(m + n + k)
+    A = rng.standard_normal((m, k)).astype(np.float32)
+    B = rng.standard_normal((k, n)).astype(np.float32)
+    bias = rng.standard_normal(n).astype(np.float32)
+    Ad = pitched(A, G.pitch(k))
+    Bd = pitched(B, n) if op == "NN" else pitched(np.ascontiguousarray(B.T), k)
+    code = G.OP_NN if op == "NN" else G.OP_NT
+    out = []
+    for groups in ("auto", "1"):
+        if groups == "1":
+            monkeypatch.setenv("GCN_ROWS_GROUPS", "1")
+        C = pitched(np.full((m, n), np.nan, np.float32), G.pitch(n))
+        G.gemm(code, Ad, Bd, C, bias=dev(bias), epi=G.EPI_RELU)
+        out.append(host(C).copy())
+    ref = np.maximum(A.astype(np.float64) @ B.astype(np.float64) + bias, 0)
+    mag = np.abs(A.astype(np.float64)) @ np.abs(B.astype(np.float64)) + np.abs(bias)
+    assert_mag_close(out[0], ref, mag, f"column groups {op} {shape}")
+    np.testing.assert_array_equal(out[0], out[1])
+
+
 @pytest.mark.parametrize("op,n,k,epi", [("NN", 256, 256, "none"), ("NT", 256, 256, "mask"), ("NN", 40, 256, "none"),
                                         ("NT", 256, 40, "mask"), ("NN", 256, 128, "relu")])
 def test_gemm_row_panels_full_size(G, op, n, k, epi):

@@ -431,6 +431,23 @@ def test_epoch_bitwise_deterministic(G, small):
         assert torch.equal(a, b)
 
 
+def test_epoch_column_groups_are_exact(G, small, monkeypatch):
+    """The short-k input gradient (width 40 -> 256, with the bitmask and the fused bias
+    gradient) split over two column groups gives bitwise the same epoch as one group."""
+    monkeypatch.setenv("GCN_GEMM_ROWS", "1")
+    p = small
+    outs = []
+    for groups in ("auto", "1"):
+        monkeypatch.setenv("GCN_ROWS_GROUPS", groups)
+        m = G.Model(p.wl.n, p.wl.widths, p.Ws, p.bs)
+        for _ in range(2):
+            m.epoch(p.dg, X=dev(p.X), labels=dev(p.y))
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in m.W + m.b + m.dW + m.db + [m.loss]])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 @pytest.mark.parametrize("rows", ["auto", "1"])
 def test_epoch_prep_is_exact(G, small, rows, monkeypatch):
     """The epoch's weight split at its start (one launch for every row-panel product) and
