@@ -56,6 +56,8 @@ struct RowsArgs {
   int64_t nslab;
   int c_vec;         // C rows 16-byte aligned with ldc % 4 == 0
   float* part;       // p.colsum: per-workgroup column sums [workgroups][n]
+  int groups;        // column groups (1 or 2): workgroups per row panel
+  int64_t panels;    // row panels of 128 rows
 };
 
 // Thread i of a split of B (k x n, or its transpose stored n x k): 8 values of B for one
@@ -144,10 +146,20 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   const int tid = threadIdx.x, l = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);  // wave-uniform: scalar registers
   const int h = l / 32, l32 = l % 32;
-  const int64_t row0 = (int64_t)blockIdx.x * kRowsPerBlock + (int64_t)wave * kRowsPerWave;
-  // column group: tiles jb .. jb + NJ - 1 of the r.nj column tiles (one group unless the
-  // launch splits the columns over blockIdx.y)
-  const int jb = (int)blockIdx.y * NJ;
+  // Row panel and column group (tiles jb .. jb + NJ - 1 of the r.nj column tiles).  With
+  // two groups, workgroup ids (dealt to the 8 XCDs in turn: id % 8 is the XCD) are mapped
+  // so that the two groups of a panel run on one XCD, eight ids apart, and the second
+  // reads the panel's rows of A from that XCD's L2.
+  int64_t panel = blockIdx.x;
+  int grp = 0;
+  if (r.groups == 2) {
+    const int64_t t = (int64_t)blockIdx.x / 8;
+    panel = (t / 2) * 8 + blockIdx.x % 8;
+    grp = (int)(t % 2);
+    if (panel >= r.panels) return;  // the whole workgroup: no barrier has been reached
+  }
+  const int64_t row0 = panel * kRowsPerBlock + (int64_t)wave * kRowsPerWave;
+  const int jb = grp * NJ;
   const int64_t cb = (int64_t)jb * 32;
   const int64_t nslab = r.nslab, nstep = 2 * nslab;
 
@@ -378,15 +390,15 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
         float v = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) v += ws[w * kMaxN + t];
-        r.part[(int64_t)blockIdx.x * p.n + t] = v;
+        r.part[panel * p.n + t] = v;
       }
     }
   }
 }
 
 template <int NJ, int PD>
-void launch_nj(const RowsArgs& r, hipStream_t s, unsigned groups = 1) {
-  const dim3 grid((unsigned)ceil_div(r.p.m, kRowsPerBlock), groups);
+void launch_nj(const RowsArgs& r, hipStream_t s) {
+  const dim3 grid((unsigned)(r.groups == 2 ? ceil_div(r.panels, 8) * 16 : r.panels));
   switch (r.p.epi) {
     case GEMM_RELU: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_RELU>), grid, dim3(kThreads), 0, s, r); break;
     case GEMM_MASK: hipLaunchKernelGGL((k_gemm_rows<NJ, PD, GEMM_MASK>), grid, dim3(kThreads), 0, s, r); break;
@@ -450,15 +462,21 @@ gcn_status launch_gemm_rows(const GemmParams& p, void* ws, hipStream_t s) {
                        static_cast<__bf16*>(ws));
     GCN_TRY(check_launch("gemm weight split"));
   }
-  // With a short k the matrix work is small and the epilogue (every column of 32 rows per
-  // wavefront) dominates; with fewer than 2048 row panels (8 per CU) the last wave of
-  // workgroups also leaves CUs idle.  Then 8 column tiles go to two workgroups of 4 each
-  // (half the accumulators per wavefront, twice the workgroups), which read A twice.
-  // Measured on the width-40 input gradient: 169,343 rows 81.2 -> 72.3 us; at 2,449,029
-  // rows (19,133 panels) 0.80 -> 0.82 ms, so not there.  GCN_ROWS_GROUPS=1 keeps one group.
+  // With fewer than 2048 row panels (8 per CU) the last wave of workgroups leaves CUs
+  // idle, and with a short k the epilogue (every column of 32 rows per wavefront)
+  // dominates.  There the 8 column tiles go to two workgroups of 4 each: half the
+  // accumulators per wavefront and twice the workgroups, the second reading the panel's
+  // rows of A from L2.  Measured on the arxiv-like products (169,343 rows, 1,323 panels):
+  // width-40 input gradient 81.2 -> 72.3 us, 128 -> 256 transform 107 -> 100 us, masked
+  // 256 x 256 input gradient 153 -> 149 us, 256 x 256 transform 135.5 -> 138 us; epoch
+  // 2.179 -> 2.153 ms.  At 2,449,029 rows (19,133 panels) the width-47 input gradient
+  // measured 0.80 -> 0.82 ms, so not there.  GCN_ROWS_GROUPS=1 / =2 force one / two.
   const char* ge = getenv("GCN_ROWS_GROUPS");
-  const bool grouped = r.nj == 8 && p.k <= 64 && ceil_div(p.m, kRowsPerBlock) < 2048 && !(ge && strcmp(ge, "1") == 0);
-  if (grouped) launch_nj<4, 2>(r, s, 2);
+  r.panels = ceil_div(p.m, kRowsPerBlock);
+  const bool grouped = r.nj == 8 && !(ge && strcmp(ge, "1") == 0) &&
+                       (r.panels < 2048 || (ge && strcmp(ge, "2") == 0));
+  r.groups = grouped ? 2 : 1;
+  if (grouped) launch_nj<4, 2>(r, s);
   else switch (r.nj) {
     case 1: launch_nj<1, 3>(r, s); break;
     case 2: launch_nj<2, 3>(r, s); break;

@@ -329,9 +329,10 @@ def test_gemm_row_panels(G, op, shape, monkeypatch):
 
 
 @pytest.mark.parametrize("op", ["NN", "NT"])
-@pytest.mark.parametrize("shape", [(600, 256, 33), (4099, 250, 40), (300, 226, 64)], ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("shape", [(600, 256, 33), (4099, 250, 40), (300, 226, 64), (1025, 256, 256), (777, 240, 130)],
+                         ids=lambda s: "x".join(map(str, s)))
 def test_gemm_row_panels_column_groups(G, op, shape, monkeypatch):
-    """Short k: the 8 column tiles go to two workgroups of 4; every output element keeps
+    """Few row panels: the 8 column tiles go to two workgroups of 4; every output element keeps
     its summation order, so the result equals the one-group launch bit for bit."""
     monkeypatch.setenv("GCN_GEMM_ROWS", "1")
     m, n, k = shape
