@@ -213,6 +213,8 @@ def test_sparse_weight_gradient_row_chunks(G, orc, w, monkeypatch):
         C2 = torch.full((F, w), float("nan"), device="cuda")
         G.spmm_xt(sx, dev(Gr), C2)
         out[xt + " (gcn_spmm_xt)"] = host(C2)
+        G.spmm_xt(sx, dev(Gr), C2)
+        np.testing.assert_array_equal(host(C2), out[xt + " (gcn_spmm_xt)"])  # fixed order
     ref = orc.matmul(X.T, Gr)
     mag = orc.matmul(np.abs(X).T, np.abs(Gr))
     for xt, got in out.items():
