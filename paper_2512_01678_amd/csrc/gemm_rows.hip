@@ -289,14 +289,16 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
   // between stores also waits for those stores, and loads inside the store loop would
   // serialise it on store completion.
   constexpr int kPairs = (NJ + 1) / 2;
+  // this workgroup's columns end at ce (a pair may run past a group's last tile)
+  const int64_t ce = cb + NJ * 32 < p.n ? cb + NJ * 32 : p.n;
   float bias_all[kPairs][4];
   uint32_t mask_all[kPairs][EPI == GEMM_MASK ? 8 : 1];
 #pragma unroll
   for (int jp = 0; jp < kPairs; ++jp) {
     const int64_t col = cb + (int64_t)jp * 64 + sc;
-    const bool cin = col < p.n;
+    const bool cin = col < ce;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) bias_all[jp][q] = p.bias && cin && col + q < p.n ? p.bias[col + q] : 0.f;
+    for (int q = 0; q < 4; ++q) bias_all[jp][q] = p.bias && cin && col + q < ce ? p.bias[col + q] : 0.f;
     if constexpr (EPI == GEMM_MASK) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -319,7 +321,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
     // the fence keeps the compiler from reordering them
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     const int64_t col = cb + (int64_t)j0 * 32 + sc;
-    const bool cin = col < p.n, full = col + 4 <= p.n;
+    const bool cin = col < ce, full = col + 4 <= ce;
     const float* bias = bias_all[j0 / 2];
     // bitmask words: 8 lanes (32 columns) per word; the lanes of a word share the row
     const int64_t word = col / 32;
@@ -338,7 +340,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
           uint32_t bits = 0;
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            if (col + q < p.n && v[q] > 0.f) bits |= 1u << (shift + q);
+            if (col + q < ce && v[q] > 0.f) bits |= 1u << (shift + q);
           bits = group_or<8>(bits);
           if (rin && cin && l % 8 == 0) p.relu_bits[row * p.ld_relu_bits + word] = bits;
         }
@@ -359,7 +361,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
       } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          if (col + q < p.n) cp[q] = v[q];
+          if (col + q < ce) cp[q] = v[q];
       }
     }
     if constexpr (EPI == GEMM_MASK) {
@@ -375,7 +377,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
         if (sr == 0 && cin)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            if (col + q < p.n) ws[q] = cs[q];
+            if (col + q < ce) ws[q] = cs[q];
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // before the next pair's writes
@@ -385,7 +387,6 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2
       // the workgroup's partial row: the wavefronts' sums of column t, in wavefront order
       __syncthreads();
       const float* ws = reinterpret_cast<const float*>(lds) + kWaves * kRowsPerWave * kStagePitch;
-      const int64_t ce = cb + NJ * 32 < p.n ? cb + NJ * 32 : p.n;
       for (int64_t t = cb + tid; t < ce; t += kThreads) {
         float v = 0.f;
 #pragma unroll
