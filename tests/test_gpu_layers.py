@@ -316,6 +316,32 @@ def test_epochs_dense_path_aggregate_first(G, orc, small, rows, monkeypatch):
     assert m.orders()[0] == G.AGGREGATE_FIRST and m.orders()[1] == G.TRANSFORM_FIRST
 
 
+# The Reddit-shaped and products-shaped models (Table II widths, the generator's degree
+# distribution) on graphs small enough for whole-epoch oracle runs: reddit-like keeps
+# a high mean degree (200 here, about 490 at full size) and its 602-wide input makes
+# layer 0 transform-first; products-like has the aggregate-first 100-wide layer 0 and a
+# 47-class loss.
+SHAPED = {
+    "reddit_like": (6000, 600000),
+    "products_like": (20000, 500000),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SHAPED))
+@pytest.mark.parametrize("rows", ["auto", "1"])
+def test_epochs_workload_shapes(G, orc, name, rows, monkeypatch):
+    """rows=1: the row-panel products used at full size, forced below their automatic
+    row threshold."""
+    if rows != "auto":
+        monkeypatch.setenv("GCN_GEMM_ROWS", rows)
+    n, e = SHAPED[name]
+    p = Problem(G, orc, gs.scaled(gs.WORKLOADS[name], n, e, name=f"{name}_scaled"))
+    m = run_epochs(G, orc, p, 2, sparse=False)
+    want = {"reddit_like": [G.TRANSFORM_FIRST, G.TRANSFORM_FIRST],
+            "products_like": [G.AGGREGATE_FIRST, G.TRANSFORM_FIRST, G.TRANSFORM_FIRST]}[name]
+    assert m.orders() == want
+
+
 @pytest.fixture(scope="module")
 def tiny(G, orc):
     wl = gs.scaled(gs.WORKLOADS["arxiv_like"], 3000, 15000, name="arxiv_like_tiny")
