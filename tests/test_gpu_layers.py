@@ -561,6 +561,29 @@ def test_epoch_rmat_4096_features_sparse(G, orc, xt, monkeypatch):
     run_epochs(G, orc, p, 1, sparse=True)
 
 
+@pytest.mark.parametrize("density", [0.5, 0.01, 0.001])
+def test_epoch_rmat_4096_features_densities(G, orc, density):
+    """The rest of the RMAT sweep's densities on 2^14 nodes: the probe picks the dense
+    path at 50 % and the sparse one below; one epoch against the oracle."""
+    from gcn_synth import device
+    wl = gs.Workload(f"rmat14_p{density}", 1 << 14, "rmat", 1 << 18, (4096, 128, 32), "nonneg", density,
+                     rmat_scale=14)
+    s, d = gs.rmat(14, 1 << 18)
+    n = wl.n
+    Xd = torch.zeros((n, 4096), device="cuda")
+    device.bernoulli_into(Xd, density, seed=0, stream=3)
+    X = gs.features_bernoulli(n, 4096, density, seed=0, stream=3, binary=False)
+    info, sx = G.feature_stats(Xd)
+    assert info["nnz"] == np.count_nonzero(X)
+    sparse = density < 0.2
+    assert info["mode"] == (G.SPARSE if sparse else G.DENSE)
+    p = Problem.__new__(Problem)
+    p.wl, p.og, p.dg = wl, orc.build_csr(n, s, d), G.build_csr(n, dev(s), dev(d))
+    p.X, p.y = X, gs.labels(n, 32)
+    p.Ws, p.bs = gs.make_weights(wl)
+    run_epochs(G, orc, p, 1, sparse=sparse)
+
+
 # ---------------------------------------------------------------------------
 # degenerate cases of the method
 # ---------------------------------------------------------------------------
