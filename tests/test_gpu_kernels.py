@@ -405,20 +405,30 @@ def test_gemm_tn_ragged(G, m, n, k):
 # ---------------------------------------------------------------------------
 
 
-@pytest.mark.parametrize("rows,w", [(169343, 256), (2708, 7), (1000, 300), (5, 1), (0, 3)])
-def test_column_sums(G, rows, w):
+@pytest.mark.parametrize("rows,w", [(169343, 256), (2708, 7), (1000, 300), (8192, 40), (8193, 40), (5, 1),
+                                    (0, 3)])
+@pytest.mark.parametrize("with_rv", [True, False])
+def test_column_sums(G, rows, w, with_rv):
+    """Column sums with and without the per-row values' mean (the loss pass's form and the
+    plain bias gradient share one summation order)."""
     rng = np.random.default_rng(rows + w)
     Gm = rng.standard_normal((rows, w)).astype(np.float32)
     rv = rng.random(rows).astype(np.float32)
-    out = torch.empty(max(w, 1), dtype=torch.float32, device="cuda")
+    out = torch.full((max(w, 1),), float("nan"), dtype=torch.float32, device="cuda")
     mean = torch.empty(1, dtype=torch.float32, device="cuda")
-    G.column_sums(pitched(Gm, G.pitch(w)), out[:w], row_vals=dev(rv) if rows else None,
-                  mean=mean if rows else None)
+    use_rv = with_rv and rows > 0
+    G.column_sums(pitched(Gm, G.pitch(w)), out[:w], row_vals=dev(rv) if use_rv else None,
+                  mean=mean if use_rv else None)
     want = Gm.astype(np.float64).sum(0)
     mag = np.abs(Gm.astype(np.float64)).sum(0)
     assert_mag_close(host(out)[:w], want, mag, "column sums")
-    if rows:
+    if use_rv:
         assert host(mean)[0] == pytest.approx(rv.astype(np.float64).mean(), rel=1e-6)
+    # fixed summation order: a second call gives the same bits
+    again = torch.empty_like(out)
+    G.column_sums(pitched(Gm, G.pitch(w)), again[:w], row_vals=dev(rv) if use_rv else None,
+                  mean=torch.empty_like(mean) if use_rv else None)
+    assert torch.equal(out[:w], again[:w])
 
 
 def test_adam(G, orc):
