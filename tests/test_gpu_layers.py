@@ -222,6 +222,35 @@ def test_sparse_weight_gradient_row_chunks(G, orc, w, monkeypatch):
     assert np.all(out["tiled"][5] == 0.0)
 
 
+@pytest.mark.parametrize("case", ["exact_chunks", "last_chunk_only", "one_row", "no_entries"])
+def test_spmm_xt_chunk_edges(G, orc, case, monkeypatch):
+    """X_csc^T Q at the edges of the row chunking, plain and tiled: a row count that is an
+    exact multiple of the chunk, entries only in the last (ragged) chunk, a single row,
+    and an all-zero X (nnz = 0: the result is exactly zero)."""
+    rng = np.random.default_rng(23)
+    n, F, w = {"exact_chunks": (2 * 8192, 300, 40), "last_chunk_only": (2 * 8192 + 100, 64, 33),
+               "one_row": (1, 50, 16), "no_entries": (8192 + 1, 40, 8)}[case]
+    X = np.where(rng.random((n, F)) < 0.05, rng.standard_normal((n, F)), 0.0).astype(np.float32)
+    if case == "last_chunk_only":
+        X[:2 * 8192] = 0.0
+    if case == "one_row":
+        X[0, ::10] = 1.5
+    if case == "no_entries":
+        X[:] = 0.0
+    info, sx = G.feature_stats(dev(X))
+    assert info["mode"] == G.SPARSE and info["nnz"] == np.count_nonzero(X)
+    Q = rng.standard_normal((n, w)).astype(np.float32)
+    ref = orc.matmul(X.T, Q)
+    mag = orc.matmul(np.abs(X).T, np.abs(Q))
+    for xt in ("plain", "tiled"):
+        monkeypatch.setenv("GCN_XT", xt)
+        C2 = torch.full((F, w), float("nan"), device="cuda")
+        G.spmm_xt(sx, pad(G, Q), C2)
+        got = host(C2)
+        assert_mag_close(got, ref, mag, f"X^T Q {case} ({xt})")
+        assert np.all(got[np.abs(X).sum(0) == 0] == 0.0)  # empty columns give exact zeros
+
+
 # ---------------------------------------------------------------------------
 # whole epochs (end-to-end parity, determinism)
 # ---------------------------------------------------------------------------
