@@ -430,33 +430,57 @@ __global__ void __launch_bounds__(WM* WN * 64) k_gemm(GemmArgs g) {
   }
 }
 
-// C(m,n) = sum_s part[s](m,n) (+ bias).  A workgroup owns 64 consecutive output
-// elements; its 4 split lanes sum the partials s = lane, lane + 4, ... in increasing
-// order and are then combined in lane order, so the rounding is fixed.
+// C(m,n) = sum_s part[s](m,n) (+ bias).  A workgroup owns kRedElems = 256 / SL
+// consecutive output elements; its SL split lanes sum the partials s = lane, lane + SL,
+// ... in increasing order into four interleaved accumulators, and the SL lane sums are
+// combined by a fixed binary tree, so the rounding is fixed.  SL = 4 reads 256-byte
+// segments of each partial; SL = 16 (64-byte segments) keeps each lane's chain of
+// dependent loads short when the output is small and the splits are many (the 256 x 40
+// weight gradient sums 512 partials).
+template <int SL>
 __global__ void __launch_bounds__(256) k_splitk_reduce(const float* part, int64_t splits, int64_t m,
                                                        int64_t n, float* C, int64_t ldc,
                                                        const float* bias) {
-  __shared__ float red[4][64];
-  const int e = threadIdx.x % 64, sl = threadIdx.x / 64;
-  const int64_t i = (int64_t)blockIdx.x * 64 + e;
+  constexpr int kRedLanes = SL, kRedElems = 256 / SL;
+  __shared__ float red[kRedLanes][kRedElems];
+  const int e = threadIdx.x % kRedElems, sl = threadIdx.x / kRedElems;
+  const int64_t i = (int64_t)blockIdx.x * kRedElems + e;
   const int64_t mn = m * n;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   if (i < mn) {
     int64_t z = sl;
-    for (; z + 12 < splits; z += 16) {
+    for (; z + 3 * kRedLanes < splits; z += 4 * kRedLanes) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) acc[u] += part[(z + 4 * u) * mn + i];
+      for (int u = 0; u < 4; ++u) acc[u] += part[(z + kRedLanes * u) * mn + i];
     }
-    for (; z < splits; z += 4) acc[0] += part[z * mn + i];
+    for (; z < splits; z += kRedLanes) acc[0] += part[z * mn + i];
   }
   red[sl][e] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
   __syncthreads();
+  for (int o = kRedLanes / 2; o > 0; o >>= 1) {
+    if (sl < o) red[sl][e] += red[sl + o][e];
+    __syncthreads();
+  }
   if (sl == 0 && i < mn) {
-    float s = ((red[0][e] + red[1][e]) + red[2][e]) + red[3][e];
+    float s = red[0][e];
     const int64_t row = i / n, col = i % n;
     if (bias) s += bias[col];
     C[row * ldc + col] = s;
   }
+}
+
+// Launch of k_splitk_reduce: 16 split lanes when the 4-lane form would leave the CUs with
+// fewer than two workgroups each.
+gcn_status launch_reduce(const float* part, int64_t splits, int64_t m, int64_t n, float* C, int64_t ldc,
+                         const float* bias, hipStream_t s) {
+  const int64_t total = m * n;
+  if (ceil_div(total, 64) < 512)
+    hipLaunchKernelGGL(k_splitk_reduce<16>, dim3((unsigned)ceil_div(total, 16)), dim3(256), 0, s, part, splits, m, n,
+                       C, ldc, bias);
+  else
+    hipLaunchKernelGGL(k_splitk_reduce<4>, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, part, splits, m, n,
+                       C, ldc, bias);
+  return check_launch("split-k reduce");
 }
 
 }  // namespace
@@ -465,9 +489,7 @@ gcn_status launch_partial_sum(const float* part, int64_t splits, int64_t m, int6
                               hipStream_t s) {
   const int64_t total = m * n;
   if (total == 0) return GCN_OK;
-  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, part, splits, m, n, C,
-                     ldc, nullptr);
-  return check_launch("partial sum");
+  return launch_reduce(part, splits, m, n, C, ldc, nullptr, s);
 }
 
 namespace {
@@ -601,10 +623,7 @@ gcn_status launch_gemm(const GemmParams& p, void* ws, hipStream_t s) {
   else if (p.ta && !p.tb) st = launch_layout<true, false>(g, sh, splits, emu, s);
   else st = launch_layout<true, true>(g, sh, splits, emu, s);
   if (st != GCN_OK || splits == 1) return st;
-  const int64_t total = p.m * p.n;
-  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)ceil_div(total, 64)), dim3(256), 0, s, g.part,
-                     splits, p.m, p.n, p.C, p.ldc, p.bias);
-  return check_launch("gemm split-k reduce");
+  return launch_reduce(g.part, splits, p.m, p.n, p.C, p.ldc, p.bias, s);
 }
 
 // ---------------------------------------------------------------------------
