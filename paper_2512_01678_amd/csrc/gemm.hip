@@ -635,23 +635,28 @@ constexpr int kColBlocksMax = 1024;
 int col_blocks(int64_t rows) { return (int)std::max<int64_t>(1, std::min<int64_t>(kColBlocksMax, ceil_div(rows, 64))); }
 
 // Workgroup b sums rows [b*chunk, (b+1)*chunk).  Thread (c4, rl): columns 4*c4 .. 4*c4+3
-// of each 256-column slab, rows rl, rl+4, ...; the 4 row lanes are combined in order.
+// of each 4*CQ-column slab, rows rl, rl + RL, ... (RL = 256 / CQ row lanes); the row
+// lanes are combined in lane order.  CQ = 64 for wide matrices; CQ = 16 for at most 64
+// columns, where 64 column lanes would leave most threads idle and each busy one a long
+// chain of row loads (the loss layer's 40 columns).
+template <int CQ>
 __global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w, const float* G, int64_t ldg,
                                                         int64_t chunk, const float* rv, double* part,
                                                         int32_t pw, int vec) {
-  __shared__ double red[4][256];
-  const int c4 = threadIdx.x % 64, rl = threadIdx.x / 64;
+  constexpr int RL = 256 / CQ;
+  __shared__ double red[RL][4 * CQ];
+  const int c4 = threadIdx.x % CQ, rl = threadIdx.x / CQ;
   const int64_t r0 = (int64_t)blockIdx.x * chunk;
   const int64_t r1 = r0 + chunk < rows ? r0 + chunk : rows;
-  for (int cb = 0; cb < w; cb += 256) {
+  for (int cb = 0; cb < w; cb += 4 * CQ) {
     const int c = cb + 4 * c4;
     float a[4] = {0.f, 0.f, 0.f, 0.f}, b[4] = {0.f, 0.f, 0.f, 0.f};
     if (c < w) {
       if (vec && c + 4 <= w) {
         int64_t r = r0 + rl;
-        for (; r + 4 < r1; r += 8) {
+        for (; r + RL < r1; r += 2 * RL) {
           const float4 x = *reinterpret_cast<const float4*>(G + r * ldg + c);
-          const float4 y = *reinterpret_cast<const float4*>(G + (r + 4) * ldg + c);
+          const float4 y = *reinterpret_cast<const float4*>(G + (r + RL) * ldg + c);
           a[0] += x.x; a[1] += x.y; a[2] += x.z; a[3] += x.w;
           b[0] += y.x; b[1] += y.y; b[2] += y.z; b[3] += y.w;
         }
@@ -660,7 +665,7 @@ __global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w,
           a[0] += x.x; a[1] += x.y; a[2] += x.z; a[3] += x.w;
         }
       } else {
-        for (int64_t r = r0 + rl; r < r1; r += 4)
+        for (int64_t r = r0 + rl; r < r1; r += RL)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             if (c + i < w) a[i] += G[r * ldg + c + i];
@@ -672,22 +677,26 @@ __global__ void __launch_bounds__(256) k_colsum_partial(int64_t rows, int32_t w,
     if (rl == 0) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (c + i < w)
-          part[(int64_t)blockIdx.x * pw + c + i] =
-              ((red[0][4 * c4 + i] + red[1][4 * c4 + i]) + red[2][4 * c4 + i]) + red[3][4 * c4 + i];
+        if (c + i < w) {
+          double t = red[0][4 * c4 + i];
+#pragma unroll
+          for (int q = 1; q < RL; ++q) t += red[q][4 * c4 + i];
+          part[(int64_t)blockIdx.x * pw + c + i] = t;
+        }
     }
     __syncthreads();
   }
   if (rv) {
+    double* flat = &red[0][0];  // 1024 doubles
     double s = 0.0;
     for (int64_t r = r0 + threadIdx.x; r < r1; r += 256) s += (double)rv[r];
-    red[0][threadIdx.x] = s;
+    flat[threadIdx.x] = s;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
-      if ((int)threadIdx.x < o) red[0][threadIdx.x] += red[0][threadIdx.x + o];
+      if ((int)threadIdx.x < o) flat[threadIdx.x] += flat[threadIdx.x + o];
       __syncthreads();
     }
-    if (threadIdx.x == 0) part[(int64_t)blockIdx.x * pw + w] = red[0][0];
+    if (threadIdx.x == 0) part[(int64_t)blockIdx.x * pw + w] = flat[0];
   }
 }
 
@@ -733,8 +742,12 @@ gcn_status launch_colsum(int64_t rows, int32_t w, const float* G, int64_t ldg, f
   const int64_t chunk = rows > 0 ? ceil_div(rows, nblk) : 1;
   double* part = static_cast<double*>(ws);
   const int vec = G && ldg % 4 == 0 && aligned16(G);
-  hipLaunchKernelGGL(k_colsum_partial, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
-                     part, pw, vec);
+  if (w <= 64)
+    hipLaunchKernelGGL(k_colsum_partial<16>, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
+                       part, pw, vec);
+  else
+    hipLaunchKernelGGL(k_colsum_partial<64>, dim3(nblk), dim3(256), 0, s, rows, w, G, ldg, chunk, row_vals,
+                       part, pw, vec);
   GCN_TRY(check_launch("column sums"));
   hipLaunchKernelGGL(k_colsum_final, dim3((unsigned)ceil_div(pw, 4)), dim3(256), 0, s, part, nblk, w, pw,
                      out, mean, rows > 0 ? 1.0 / (double)rows : 0.0);
