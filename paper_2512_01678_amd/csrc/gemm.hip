@@ -511,13 +511,17 @@ Shape pick_shape(const GemmParams& p, bool emu) {
   return {128, 128};
 }
 
+#ifndef GCN_TN_WAVES
+#define GCN_TN_WAVES 2048  // wavefronts of a split-k A^T B launch
+#endif
+
 int64_t pick_splits(const GemmParams& p, Shape sh) {
   if (!p.ta) return 1;  // only A^T B reduces over the long (row) dimension
   // about 2048 wavefronts in all (measured best for wide and narrow tiles alike), each
   // workgroup walking at least 256 rows of k
   const int64_t tiles = ceil_div(p.m, sh.bm) * ceil_div(p.n, sh.bn);
   const int64_t waves = sh.bn >= 256 ? 8 : (sh.bn >= 128 ? 4 : sh.bm / 64);
-  int64_t s = ceil_div(2048, tiles * waves);
+  int64_t s = ceil_div(GCN_TN_WAVES, tiles * waves);
   const int64_t max_s = ceil_div(p.k, 256);
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;
