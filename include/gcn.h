@@ -26,8 +26,10 @@
  *    asynchronous and report launch errors as GCN_E_HIP.
  *  - No exception crosses this interface.  gcn_last_error() returns a
  *    thread-local message describing the last failure on the calling thread.
- *  - Results are deterministic: no floating-point atomics are used, so two
- *    runs on the same inputs give bitwise-equal outputs.
+ *  - Results are deterministic on the default path: it uses no floating-point
+ *    atomics, so two runs on the same inputs give bitwise-equal outputs.  The one
+ *    exception is the sparse backward without a CSC view (gcn_layer_bwd), an
+ *    ablation that adds with fp32 atomics.
  */
 #ifndef GCN_H_
 #define GCN_H_
@@ -155,7 +157,9 @@ typedef struct gcn_layer {
   int32_t f_in, f_out;  /* widths of H_in and H_out */
   int64_t ld_in;        /* pitch of H_in and of the saved aggregate of H_in (aggregate-first) */
   int64_t ld_out;       /* pitch of H_out / Z and of G = dLoss/dZ */
-  int32_t act;          /* GCN_ACT_RELU (hidden), GCN_ACT_NONE, GCN_ACT_SOFTMAX_CE (last) */
+  int32_t act;          /* GCN_ACT_RELU (hidden), GCN_ACT_NONE, GCN_ACT_SOFTMAX_CE (last);
+                           gcn_epoch takes ReLU on every hidden layer (GCN_E_UNSUPPORTED
+                           otherwise) and softmax cross-entropy on the last */
   int32_t order;        /* GCN_ORDER_AUTO or a forced evaluation order */
   int32_t index;        /* layer number l (0 = input layer) */
   int32_t agg;          /* GCN_AGG_NORM (0), GCN_AGG_SUM, GCN_AGG_MEAN or GCN_AGG_MAX */

@@ -1,7 +1,7 @@
 // adam.hip -- one fused Adam step over every parameter tensor of the model.
 //
-// Listing 1 ends each epoch with optimizer("adam", 0.01, 0.9, 0.999); the
-// update is the bias-corrected Adam rule
+// Listing 1 ends each epoch with an Adam step (learning rate 0.01, first- and
+// second-moment decay 0.9 and 0.999); the update is the bias-corrected Adam rule
 //   m = b1 m + (1-b1) g,  v = b2 v + (1-b2) g^2,
 //   p = p - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps),
 // applied elementwise.  All tensors go in one launch (their pointers travel

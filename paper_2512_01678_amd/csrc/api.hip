@@ -566,6 +566,10 @@ gcn_status gcn_epoch(gcn_model* m, const gcn_graph* g, const float* d_X, const g
       return fail(GCN_E_INVALID, "gcn_epoch: consecutive layer widths / pitches disagree");
     if ((l == L - 1) != (ly->act == GCN_ACT_SOFTMAX_CE))
       return fail(GCN_E_INVALID, "gcn_epoch: softmax cross-entropy must be the last layer's activation");
+    // the backward of layer l + 1 multiplies by 1[H_{l+1} > 0], the derivative of ReLU,
+    // so a hidden layer without it would get wrong gradients
+    if (l < L - 1 && ly->act != GCN_ACT_RELU)
+      return fail(GCN_E_UNSUPPORTED, "gcn_epoch: every hidden layer's activation must be ReLU");
     if (!m->W[l] || !m->dW[l] || !m->db[l] || !m->mW[l] || !m->vW[l] || !m->grad[l] || !m->b[l] ||
         !m->mb[l] || !m->vb[l] || (l < L - 1 && !m->act[l]))
       return fail(GCN_E_INVALID, "gcn_epoch: a layer buffer is NULL");

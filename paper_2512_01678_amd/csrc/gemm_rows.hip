@@ -1,7 +1,7 @@
 // gemm_rows.hip -- C = A B for a tall A and a small B (n <= 256), bf16x6 arithmetic.
 //
 // The transform products of a GCN layer multiply an N x k feature matrix by a k x n
-// weight (H W forward, Q W^T for the input gradient, Section II-A / Algorithm 1), with N
+// weight (H W forward, Q W^T for the input gradient, Section III-A / Algorithm 1), with N
 // in the hundreds of thousands and k, n at most a few hundred.  The general tiled GEMM
 // re-splits the weight in every workgroup and reads each row of A once per 128 output
 // columns; here instead:

@@ -205,3 +205,31 @@ def test_order_rule(G):
     assert G.layer_order(128, 256, 0, G.ACT_RELU, x_sparse=True) == G.TRANSFORM_FIRST
     assert G.layer_order(16, 700, 1, G.ACT_SOFTMAX_CE) == G.TRANSFORM_FIRST
     assert G.layer_order(128, 256, 0, G.ACT_RELU, order=G.TRANSFORM_FIRST) == G.TRANSFORM_FIRST
+
+
+def test_epoch_rejects_hidden_layer_without_relu(G):
+    """The backward of the layer above a hidden layer multiplies by 1[H > 0], ReLU's
+    derivative; gcn_epoch refuses a hidden layer with another activation instead of
+    producing wrong gradients.  Returns from host validation / the size query only."""
+    L = G.raw_lib()
+    n = 10
+    g = G.gcn_graph(n, 20, 20, 1, 1, 1, 1, 1)
+
+    def model(hidden_act):
+        lays = (G.gcn_layer * 2)(G.gcn_layer(8, 4, 8, 4, hidden_act, G.TRANSFORM_FIRST, 0),
+                                 G.gcn_layer(4, 3, 4, 4, G.ACT_SOFTMAX_CE, G.TRANSFORM_FIRST, 1))
+        arr = lambda: (C.c_void_p * 2)(256, 512)  # stand-in device addresses, never dereferenced
+        keep = {nm: arr() for nm in ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act", "saved", "grad")}
+        m = G.gcn_model(2, C.cast(lays, C.POINTER(G.gcn_layer)),
+                        *[C.cast(keep[nm], C.POINTER(C.c_void_p)) for nm in
+                          ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act", "saved", "grad")],
+                        0.01, 0.9, 0.999, 1e-8, 0, None)
+        return m, (lays, keep)
+
+    nb = G.sz(0)
+    m, keep = model(G.ACT_NONE)
+    assert L.gcn_epoch(C.byref(m), C.byref(g), 1024, None, 2048, 4096, None, C.byref(nb), None) == G.E_UNSUPPORTED
+    assert "ReLU" in L.gcn_last_error().decode()
+    m, keep = model(G.ACT_RELU)
+    assert L.gcn_epoch(C.byref(m), C.byref(g), 1024, None, 2048, 4096, None, C.byref(nb), None) == G.OK
+    assert nb.value > 0
