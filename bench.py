@@ -38,7 +38,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="arxiv_like")
+    ap.add_argument("--workload", default="products_like",
+                    help="products_like (the default: the largest single-GPU workload, 2,449,029 nodes), "
+                         "arxiv_like, reddit_like, cora_like, rmat21_p{0.5,0.1,0.01,0.001}")
     ap.add_argument("--tau", default="4/5", help="sparse-path threshold tau as num/den")
     ap.add_argument("--force-mode", default="auto", choices=["auto", "dense", "sparse"])
     ap.add_argument("--csc", default="on", choices=["on", "off"],
@@ -60,6 +62,12 @@ def alg_bytes_aggregate(nnz: int, rows: int, w: int) -> int:
     """Algorithmic bytes of one normalised aggregation at width w: neighbour-row gathers
     4 nnz w, column indices and entry values 8 nnz, row offsets 8 (rows + 1), output 4 rows w."""
     return 4 * nnz * w + 8 * nnz + 8 * (rows + 1) + 4 * rows * w
+
+
+def compulsory_bytes_aggregate(nnz: int, rows: int, w: int) -> int:
+    """Bytes any aggregation at width w must move at least once: the column indices 4 nnz,
+    row offsets and dinv 12 N, every input row once and the output, 8 N w."""
+    return 4 * nnz + 12 * rows + 8 * rows * w
 
 
 def sha_of(path):
@@ -128,7 +136,8 @@ def cpu_baseline(wl, s, d, X, y, Ws, bs, sparse: bool, budget_s: float):
     sec = float(np.median(times))
     return {"value": 1.0 / sec, "unit": "epochs/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(times)} full fp64 oracle epoch(s) of {wl.name} (forward, loss, backward, "
-                      f"Adam), median {sec:.3f} s/epoch"}
+                      f"Adam), median {sec:.3f} s/epoch; graph loops in plain C with OpenMP over rows, "
+                      f"dense products through numpy's fp64 matmul (multi-threaded BLAS)"}
 
 
 def main():
@@ -271,6 +280,8 @@ def main():
         if name.startswith("aggregate_w"):
             by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
             k["alg_GBps"] = round(by / (avg * 1e-3) / 1e9, 1)
+            k["compulsory_frac"] = round(compulsory_bytes_aggregate(g.nnz, f["rows"], f["width"]) /
+                                         (avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
         elif name.startswith("aggmax_bwd_w"):  # gathers dP and maximisers, mask and output rows
             w = f["width"]
             by = 8 * g.nnz * w + 4 * g.nnz + 8 * (f["rows"] + 1) + 8 * f["rows"] * w
@@ -296,11 +307,24 @@ def main():
         f = timed_dom
         avg_s = f["ms"] / f["count"] * 1e-3
         by = alg_bytes_aggregate(g.nnz, f["rows"], f["width"])
-        achieved = by / avg_s / 1e9
+        bmin = compulsory_bytes_aggregate(g.nnz, f["rows"], f["width"])
+        traffic = traffic_for(dominant, wl.name)
+        # The algorithmic bytes count every neighbour-row gather as an HBM read.  Where the
+        # gathered rows are so concentrated on hub nodes that caches serve them (the RMAT
+        # graph), that rate exceeds the HBM peak and is no bound; the roofline is then taken
+        # on the bytes the HBM counters saw, or, without counters, on the compulsory bytes.
+        basis, used = "algorithmic", by
+        if by / avg_s / 1e9 > HBM_PEAK_GBS:
+            basis, used = ("hbm_counters", traffic) if traffic else ("compulsory", bmin)
+        achieved = used / avg_s / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic_for(dominant, wl.name),
-                    "kernel": dominant, "alg_bytes_per_launch": by, "avg_launch_ms": round(avg_s * 1e3, 5),
-                    "launches_timed": f["count"]}
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                    "kernel": dominant, "basis": basis, "alg_bytes_per_launch": by,
+                    "alg_GBps": round(by / avg_s / 1e9, 1),
+                    "compulsory_bytes_per_launch": bmin,
+                    "compulsory_frac": round(bmin / avg_s / 1e9 / HBM_PEAK_GBS, 4),
+                    "traffic_frac": None if not traffic else round(traffic / avg_s / 1e9 / HBM_PEAK_GBS, 4),
+                    "avg_launch_ms": round(avg_s * 1e3, 5), "launches_timed": f["count"]}
 
     # every aggregation launch of the profiled pass: bytes-weighted achieved rate of the graph SpMM
     spmm = None
@@ -308,9 +332,11 @@ def main():
                 if k.startswith("aggregate_w")]
     if agg_fams:
         tot_b = sum(by * f["count"] for f, by in agg_fams)
+        tot_min = sum(compulsory_bytes_aggregate(g.nnz, f["rows"], f["width"]) * f["count"] for f, _ in agg_fams)
         tot_s = sum(f["ms"] for f, _ in agg_fams) * 1e-3
         spmm = {"weighted_GBps": round(tot_b / tot_s / 1e9, 1),
                 "frac": round(tot_b / tot_s / 1e9 / HBM_PEAK_GBS, 4),
+                "compulsory_frac": round(tot_min / tot_s / 1e9 / HBM_PEAK_GBS, 4),
                 "launches_per_epoch": sum(f["count"] for f, _ in agg_fams) // prof_steps}
 
     # device memory during training (allocator high-water mark from the model's creation

@@ -233,3 +233,56 @@ def test_epoch_rejects_hidden_layer_without_relu(G):
     m, keep = model(G.ACT_RELU)
     assert L.gcn_epoch(C.byref(m), C.byref(g), 1024, None, 2048, 4096, None, C.byref(nb), None) == G.OK
     assert nb.value > 0
+
+
+def _epoch_ws(G, n, nnz, widths, n_chunk=0):
+    """Workspace bytes gcn_epoch asks for (size query only: stand-in device addresses)."""
+    L = G.raw_lib()
+    nl = len(widths) - 1
+    lays = (G.gcn_layer * nl)(*[
+        G.gcn_layer(widths[l], widths[l + 1], G.pitch(widths[l]), G.pitch(widths[l + 1]),
+                    G.ACT_SOFTMAX_CE if l == nl - 1 else G.ACT_RELU, G.ORDER_AUTO, l) for l in range(nl)])
+    keep = {nm: (C.c_void_p * nl)(*[4096 * (i + 1) for i in range(nl)])
+            for nm in ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act", "saved", "grad")}
+    m = G.gcn_model(nl, C.cast(lays, C.POINTER(G.gcn_layer)),
+                    *[C.cast(keep[nm], C.POINTER(C.c_void_p)) for nm in
+                      ("W", "b", "dW", "db", "mW", "vW", "mb", "vb", "act", "saved", "grad")],
+                    0.01, 0.9, 0.999, 1e-8, 0, None)
+    sp = G.gcn_split(1 if n_chunk else 0, n_chunk, max(n_chunk, 1), 256 if n_chunk else None,
+                     256 if n_chunk else None, 256 if n_chunk else None, None)
+    g = G.gcn_graph(n, nnz, nnz, 256, 256, 256, 256, 256, sp)
+    nb = G.sz(0)
+    rc = L.gcn_epoch(C.byref(m), C.byref(g), 1 << 20, None, 2 << 20, 3 << 20, None, C.byref(nb), None)
+    assert rc == G.OK, L.gcn_last_error().decode()
+    return nb.value
+
+
+@pytest.mark.parametrize("widths", [(100, 256, 256, 47), (128, 256, 256, 40), (602, 256, 41)])
+def test_epoch_memory_has_no_edge_times_width_term(G, widths):
+    """Section V-F / Table III: the fused path keeps device memory at O(|V| F) with no
+    per-edge message tensor.  With N and the widths fixed, the epoch workspace must not grow
+    with the edge count at all (the graph itself is the caller's, 8 bytes per entry), and the
+    chunk sums of split hub rows add at most 1.5 w floats per GCN_SPLIT_CHUNK entries."""
+    n = 2_449_029
+    base = _epoch_ws(G, n, 10 * n, widths)
+    assert _epoch_ws(G, n, 100 * n, widths) == base      # 10x the entries: same workspace
+    assert _epoch_ws(G, n, 1000 * n, widths) == base
+    # a per-edge message tensor at the widest layer would be nnz * w * 4 bytes; the workspace
+    # is a few node-sized matrices
+    wmax = max(widths)
+    assert base <= 4 * n * 4 * G.pitch(wmax) + (64 << 20)
+    assert base < 10 * n * 4 * wmax  # far below one edge-sized message tensor at 10 entries per node
+    # hub rows: chunk sums are w floats per chunk of 2048 entries
+    nnz = 100 * n
+    chunks = 3 * nnz // (2 * 2048) + 1
+    with_split = _epoch_ws(G, n, nnz, widths, n_chunk=chunks)
+    assert with_split - base <= chunks * 4 * G.pitch(wmax) + 4096
+    assert (with_split - base) / nnz <= 1.5 * 4 * G.pitch(wmax) / 2048 + 1e-3
+
+
+def test_epoch_memory_scales_with_nodes(G):
+    """The workspace is linear in N at fixed widths (O(|V| F))."""
+    w = (100, 256, 256, 47)
+    a, b = _epoch_ws(G, 1_000_000, 50_000_000, w), _epoch_ws(G, 2_000_000, 50_000_000, w)
+    c = _epoch_ws(G, 4_000_000, 50_000_000, w)
+    assert (c - b) == pytest.approx(2 * (b - a), rel=0.02)

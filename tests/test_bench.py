@@ -70,3 +70,22 @@ def test_calibration_crossover_interpolation():
     c = calibrate.crossover([(0.1, 1.5), (0.01, 0.5), (0.5, 4.0)])
     assert c == pytest.approx((0.01 * 0.1) ** 0.5, rel=1e-12)
     assert calibrate.crossover([(0.1, 0.5), (0.5, 0.9)]) is None  # sparse faster everywhere
+
+
+def test_compulsory_bytes_are_below_algorithmic():
+    # indices 4 nnz, offsets and dinv 12 N, each input row once and the output 8 N w
+    assert bench.compulsory_bytes_aggregate(10, 3, 2) == 4 * 10 + 12 * 3 + 8 * 3 * 2
+    for nnz, n, w in [(2_501_829, 169_343, 256), (126_167_309, 2_449_029, 47), (5, 5, 1)]:
+        assert bench.compulsory_bytes_aggregate(nnz, n, w) <= bench.alg_bytes_aggregate(nnz, n, w)
+
+
+def test_default_workload_is_the_largest_single_gpu_config():
+    import gcn_synth as gs
+    args = sys.argv
+    try:
+        sys.argv = ["bench.py"]
+        wl = gs.WORKLOADS[bench.parse().workload]
+    finally:
+        sys.argv = args
+    assert wl.n == max(w.n for w in gs.WORKLOADS.values())
+    assert wl.name == "products_like"
