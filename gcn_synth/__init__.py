@@ -18,8 +18,11 @@ RMAT graph; the datasets themselves are not used.
 """
 from __future__ import annotations
 
+import ctypes
 import hashlib
 import math
+import os
+import subprocess
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -119,8 +122,34 @@ def permutation(n: int, seed: int, stream: int) -> np.ndarray:
     return np.argsort(keys, kind="stable").astype(np.int32)
 
 
+_HOST_LIB = None
+_HOST_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "host_gen.c")
+_HOST_SO = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsynth_host.so")
+
+
+def build_host(force: bool = True) -> str:
+    """Compile host_gen.c (the C edge sampler) into libsynth_host.so."""
+    if force or not os.path.exists(_HOST_SO):
+        tmp = _HOST_SO + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", _HOST_SRC, "-o", tmp])
+        os.replace(tmp, _HOST_SO)
+    return _HOST_SO
+
+
+def host_lib():
+    """The C edge sampler, or None when it is not built (the numpy loop then runs)."""
+    global _HOST_LIB
+    if _HOST_LIB is None and os.path.exists(_HOST_SO):
+        L = ctypes.CDLL(_HOST_SO)
+        L.synth_chung_lu_keys.restype = ctypes.c_int
+        L.synth_chung_lu_keys.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_uint64,
+                                          ctypes.c_void_p]
+        _HOST_LIB = L
+    return _HOST_LIB
+
+
 def chung_lu(n: int, e_und: int, seed: int = 0, stream: int = 1, alpha: float = 2.0 / 3.0,
-             dmax: float | None = None, permute: bool = True):
+             dmax: float | None = None, permute: bool = True, use_c: bool = True):
     """Chung-Lu power-law graph with exactly ``e_und`` distinct undirected edges.
 
     Node i gets weight (i + i0)^-alpha (degree exponent 1 + 1/alpha); i0 puts the
@@ -128,7 +157,8 @@ def chung_lu(n: int, e_und: int, seed: int = 0, stream: int = 1, alpha: float = 
     endpoints are drawn proportional to weight; self pairs are discarded and each
     pair is kept once, in (min, max) form, in sampling order, until exactly
     ``e_und`` remain.  Node ids are then randomly permuted.  Returns (src, dst)
-    int32 arrays, one entry per undirected edge.
+    int32 arrays, one entry per undirected edge.  ``use_c``: draw the pairs with the C
+    sampler when it is built (the same pairs as the numpy loop, much faster).
     """
     if e_und == 0:
         z = np.zeros(0, np.int32)
@@ -142,6 +172,14 @@ def chung_lu(n: int, e_und: int, seed: int = 0, stream: int = 1, alpha: float = 
     cdf /= cdf[-1]
     have = np.zeros(0, np.int64)
     off = 0
+    hl = host_lib() if use_c else None
+    if hl is not None:  # the same sampling rule in C (host_gen.c)
+        keys = np.empty(e_und, np.int64)
+        cdf = np.ascontiguousarray(cdf)
+        rc = hl.synth_chung_lu_keys(n, e_und, cdf.ctypes.data, stream_state(seed, stream), keys.ctypes.data)
+        if rc != 0:
+            raise MemoryError("synth_chung_lu_keys: out of host memory")
+        have = np.sort(keys)
     while have.size < e_und:
         need = e_und - have.size
         b = int(need * 1.15) + 1024

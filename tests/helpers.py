@@ -81,3 +81,39 @@ def adversarial_graphs():
     hd = np.concatenate([rng.integers(1, 700, 20000).astype(np.int32), np.zeros(20000, np.int32)])
     out.append(("dup_hub", 700, hs, hd))
     return out
+
+
+def note(msg):
+    """A progress line for long GPU tests: to stderr and appended to gpurun_out/test_progress.log
+    (a long test then shows activity while it runs)."""
+    import os
+    import sys
+    import time
+    line = f"[{time.strftime('%H:%M:%S')}] {msg}"
+    print(line, file=sys.stderr, flush=True)
+    root = os.environ.get("GRAFT_REPO_ROOT") or os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    try:
+        os.makedirs(os.path.join(root, "gpurun_out"), exist_ok=True)
+        with open(os.path.join(root, "gpurun_out", "test_progress.log"), "a") as f:
+            f.write(line + "\n")
+    except OSError:
+        pass
+
+
+def relu_flips(gpu_on, Z, mag, what, band=1e-5):
+    """ReLU decisions: the GPU's 1[H > 0] (taken on its fp32 pre-activation) against the
+    oracle's 1[Z > 0] (fp64).  Where Z is within rounding of zero both are correct; a
+    differing decision is accepted only where |Z| <= band * (the element's magnitude scale
+    sum |terms|), and the number of accepted flips must stay small.  Returns the count."""
+    gpu_on = np.asarray(gpu_on, bool)
+    Z = np.asarray(Z, np.float64)
+    mag = np.asarray(mag, np.float64)
+    differ = gpu_on != (Z > 0)
+    far = differ & (np.abs(Z) > band * mag)
+    assert not far.any(), (f"{what}: {int(far.sum())} ReLU decisions differ away from zero "
+                           f"(worst |Z|/scale {float((np.abs(Z) / np.maximum(mag, 1e-300))[far].max()):.3e})")
+    flips = int(differ.sum())
+    limit = 5 + int(1e-5 * Z.size)
+    assert flips <= limit, f"{what}: {flips} ReLU flips near zero (limit {limit})"
+    note(f"{what}: {flips} ReLU flips within {band:g} x scale of zero, of {Z.size} entries")
+    return flips

@@ -1,0 +1,231 @@
+"""Parity at the full size of every workload, in the benchmark's launch configuration.
+
+One training epoch (Algorithm 1 forward and backward, the softmax cross-entropy, Adam)
+of each full-size workload runs on the GPU exactly as bench.py runs it: X at the
+bench's pitch, the density probe with tau = 4/5 choosing the path, the CSC view for a
+sparse first layer, every product at its automatic kernel choice.  Then the fp64 oracle
+checks, from the GPU's own layer inputs (unit parity, each element against its
+magnitude scale sum |terms|):
+  * every hidden layer's output H_{l+1} (and the saved aggregate of an aggregate-first
+    layer) on about 400 random rows plus every hub row longer than GCN_SPLIT_MIN (the
+    rows the library cuts into chunks) and the 20 longest rows, with the ReLU decisions
+    that differ counted and bounded;
+  * the loss and G = dLoss/dZ of the last layer on all rows;
+  * every layer's backward from the GPU's own G_l: the full weight gradient dW_l (on the
+    RMAT workloads 128 sampled rows of dW_0 = X^T Q_0, each a sum over all 2^21 nodes),
+    the full bias gradient, and G_{l-1} on the sampled rows;
+  * the Adam step of every parameter.
+The arxiv-shaped workload is checked on every row.  These sizes reach what the small
+tests cannot: operands above 2 GiB (H of the products-shaped graph is 2.5 GB, the RMAT
+features 34 GB), split-k weight gradients over 2.45 M rows, the row-panel products
+with 19,133 row panels, hub splitting on the RMAT graph and the row-chunk-tiled
+X^T Q over 256 chunks.
+"""
+import numpy as np
+import pytest
+import torch
+
+import gcn_synth as gs
+from helpers import assert_mag_close, assert_norm_close, note, relu_flips
+
+pytestmark = pytest.mark.gpu
+
+SPLIT_MIN = 4096  # GCN_SPLIT_MIN of include/gcn.h
+
+
+@pytest.fixture(scope="module")
+def G():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2512_01678_amd.gcn as G
+    return G
+
+
+def host(t, w=None):
+    torch.cuda.synchronize()
+    a = t.detach().cpu().numpy()
+    if w is not None:
+        a = a[:, :w]
+    return a.astype(np.float64)
+
+
+def sample_rows(og, count, seed=0):
+    rng = np.random.default_rng(seed)
+    n = og.n
+    hubs = np.nonzero(og.deg > SPLIT_MIN)[0]
+    top = np.argsort(og.deg, kind="stable")[-20:]
+    return np.unique(np.concatenate([rng.integers(0, n, count), hubs, top])).astype(np.int32), hubs.size
+
+
+def neighbours(og, rows):
+    parts = [og.col_idx[og.row_ptr[r]:og.row_ptr[r + 1]] for r in rows]
+    return np.unique(np.concatenate(parts)).astype(np.int64)
+
+
+class Run:
+    """One workload set up and trained for one epoch as bench.py does it."""
+
+    def __init__(self, G, orc, wl, graph=None):
+        self.wl = wl
+        n = wl.n
+        note(f"{wl.name}: drawing inputs")
+        if graph is None:
+            s, d = gs.make_graph(wl)
+            note(f"{wl.name}: {s.size} edges drawn; oracle CSR")
+            self.og = orc.build_csr(n, s, d)
+            self.dg = G.build_csr(n, torch.from_numpy(s).cuda(), torch.from_numpy(d).cuda())
+            del s, d
+        else:
+            self.og, self.dg = graph
+        assert self.dg.nnz == self.og.nnz
+        self.on_device = n * wl.f > (1 << 28)
+        self.X = None if self.on_device else gs.make_features(wl)
+        self.y = gs.make_labels(wl)
+        self.Ws, self.bs = gs.make_weights(wl)
+        ld_x = G.pitch(wl.f)
+        self.Xd = torch.zeros((n, ld_x), dtype=torch.float32, device="cuda")
+        self.Xv = self.Xd[:, :wl.f]
+        if self.on_device:
+            from gcn_synth import device
+            device.bernoulli_into(self.Xv, wl.density, seed=0, stream=3, binary=(wl.features == "binary"))
+        else:
+            self.Xv.copy_(torch.from_numpy(self.X).cuda())
+        torch.cuda.synchronize()
+        info, self.sx = G.feature_stats(self.Xv, tau=(4, 5), force_mode=-1, csc=True)
+        self.sparse = info["mode"] == G.SPARSE
+        note(f"{wl.name}: nnz(A+I) {self.og.nnz}, probe s = {info['sparsity']:.4f} -> "
+             f"{'sparse' if self.sparse else 'dense'}; one GPU epoch")
+        self.m = G.Model(n, wl.widths, self.Ws, self.bs, x_sparse=self.sparse, ld_x=ld_x)
+        self.m.epoch(self.dg, X=None if self.sparse else self.Xv, x=self.sx,
+                     labels=torch.from_numpy(self.y).cuda())
+        torch.cuda.synchronize()
+
+    def x_rows(self, rows):
+        """Rows of X in fp64 on the host (drawn on the device for the RMAT features, by the
+        same counter stream as the host generator)."""
+        if self.X is not None:
+            return self.X[rows].astype(np.float64)
+        out = np.empty((rows.size, self.wl.f), np.float64)
+        idx = torch.from_numpy(np.asarray(rows, np.int64))
+        for r0 in range(0, rows.size, 32768):
+            sel = idx[r0:r0 + 32768].cuda()
+            out[r0:r0 + sel.numel()] = self.Xv.index_select(0, sel).cpu().numpy()
+        return out
+
+
+def check_run(G, orc, run, rows, what, x_cols=None):
+    """The oracle checks described in the module docstring; rows=None: every row."""
+    wl, og, m = run.wl, run.og, run.m
+    n, L = wl.n, m.L
+    all_rows = rows is None
+    if all_rows:
+        rows = np.arange(n, dtype=np.int32)
+    need = np.arange(n) if all_rows else neighbours(og, rows)
+    Ws = [w.astype(np.float64) for w in run.Ws]
+    bs = [b.astype(np.float64) for b in run.bs]
+    Hs = [None] + [host(a, wl.widths[l + 1]) for l, a in enumerate(m.act)]
+    flips = 0
+    # forward of every hidden layer on the sampled rows, from the GPU's own layer input
+    for l in range(L - 1):
+        note(f"{what}: forward layer {l} on {rows.size} rows ({need.size} neighbour rows)")
+        M = np.zeros((n, wl.widths[l + 1]))
+        Ma = np.zeros_like(M)
+        for b0 in range(0, need.size, 65536):  # row blocks bound the host memory of wide X
+            blk = need[b0:b0 + 65536]
+            Hin = run.x_rows(blk) if l == 0 else Hs[l][blk]
+            M[blk] = Hin @ Ws[l]
+            Ma[blk] = np.abs(Hin) @ np.abs(Ws[l])
+        del Hin
+        Z = orc.aggregate(og, M, bs[l], rows=rows)
+        mag = orc.aggregate(og, Ma, np.abs(bs[l]), rows=rows)
+        got = Hs[l + 1][rows]
+        flips += relu_flips(got > 0, Z, mag, f"{what} H_{l + 1}")
+        assert_mag_close(got, np.maximum(Z, 0), mag, f"{what} H_{l + 1}")
+        if m.saved[l] is not None:
+            Xn = np.zeros((n, wl.widths[l]))
+            Xn[need] = run.x_rows(need) if l == 0 else Hs[l][need]
+            P, pmag = orc.aggregate(og, Xn, rows=rows, want_mag=True)
+            assert_mag_close(host(m.saved[l], wl.widths[l])[rows], P, pmag, f"{what} saved aggregate {l}")
+        del M, Ma
+    # loss layer on every row
+    note(f"{what}: loss layer")
+    Zl = orc.aggregate(og, Hs[L - 1] @ Ws[L - 1], bs[L - 1])
+    lo, Gl, _ = orc.softmax_ce(Zl, run.y)
+    assert float(m.loss.cpu()[0]) == pytest.approx(lo, rel=1e-4), f"{what} loss"
+    assert_norm_close(host(m.grad[L - 1], wl.widths[L]), Gl, f"{what} G_{L - 1}")
+    del Zl, Gl
+    # backward of every layer from the GPU's own G_l
+    for l in range(L - 1, -1, -1):
+        note(f"{what}: backward layer {l}")
+        Gg = host(m.grad[l], wl.widths[l + 1])
+        Q, aQ = orc.aggregate(og, Gg, want_mag=True)
+        assert_mag_close(host(m.db[l][None, :])[0], Gg.sum(axis=0), np.abs(Gg).sum(axis=0), f"{what} db_{l}")
+        if l == 0 and x_cols is not None:
+            # sampled rows k of dW_0 = X^T Q_0: column k of X over all nodes (X >= 0 here)
+            Xc = run.Xv[:, torch.from_numpy(x_cols).cuda()].cpu().numpy().astype(np.float64)
+            assert (Xc >= 0).all()
+            assert_mag_close(host(m.dW[0])[x_cols], Xc.T @ Q, Xc.T @ aQ, f"{what} dW_0 rows")
+            del Xc
+        else:
+            Hin = run.x_rows(np.arange(n)) if l == 0 else Hs[l]
+            assert_mag_close(host(m.dW[l]), Hin.T @ Q, np.abs(Hin).T @ aQ, f"{what} dW_{l}")
+            del Hin
+        if l > 0:
+            ref = (Q[rows] @ Ws[l].T) * (Hs[l][rows] > 0)
+            mag = aQ[rows] @ np.abs(Ws[l]).T
+            assert_mag_close(host(m.grad[l - 1], wl.widths[l])[rows], ref, mag, f"{what} G_{l - 1}")
+        del Gg, Q, aQ
+    # Adam step 1 from the initial parameters with the GPU's own gradients
+    for l in range(L):
+        for nm, gnm, p0 in (("W", "dW", Ws[l]), ("b", "db", bs[l])):
+            g = host(getattr(m, gnm)[l][None] if nm == "b" else getattr(m, gnm)[l])
+            g = g[0] if nm == "b" else g
+            want, _, _ = orc.adam(p0, g, np.zeros_like(p0), np.zeros_like(p0), 1)
+            got = host(getattr(m, nm)[l][None] if nm == "b" else getattr(m, nm)[l])
+            got = got[0] if nm == "b" else got
+            assert_mag_close(got, want, np.abs(p0) + 0.01, f"{what} Adam {nm}_{l}", rtol=1e-5)
+    note(f"{what}: passed ({flips} ReLU flips near zero in total)")
+
+
+def test_full_size_arxiv_like_every_row(G, orc):
+    run = Run(G, orc, gs.WORKLOADS["arxiv_like"])
+    assert run.m.orders() == [G.AGGREGATE_FIRST, G.TRANSFORM_FIRST, G.TRANSFORM_FIRST]
+    check_run(G, orc, run, None, "arxiv_like")
+
+
+@pytest.mark.parametrize("name", ["reddit_like", "products_like"])
+def test_full_size_sampled_rows(G, orc, name):
+    run = Run(G, orc, gs.WORKLOADS[name])
+    rows, n_hubs = sample_rows(run.og, 400)
+    note(f"{name}: {rows.size} sampled rows, {n_hubs} hub rows above {SPLIT_MIN} entries")
+    want = {"reddit_like": [G.TRANSFORM_FIRST, G.TRANSFORM_FIRST],
+            "products_like": [G.AGGREGATE_FIRST, G.TRANSFORM_FIRST, G.TRANSFORM_FIRST]}[name]
+    assert run.m.orders() == want
+    check_run(G, orc, run, rows, name)
+
+
+@pytest.fixture(scope="module")
+def rmat_graph(G, orc):
+    wl = gs.WORKLOADS["rmat21_p0.5"]
+    note("rmat21: drawing 2^25 samples")
+    s, d = gs.make_graph(wl)
+    og = orc.build_csr(wl.n, s, d)
+    dg = G.build_csr(wl.n, torch.from_numpy(s).cuda(), torch.from_numpy(d).cuda())
+    return og, dg
+
+
+@pytest.mark.parametrize("density", [0.5, 0.1, 0.01, 0.001])
+def test_full_size_rmat(G, orc, rmat_graph, density):
+    wl = gs.WORKLOADS[f"rmat21_p{density:g}"]
+    run = Run(G, orc, wl, graph=rmat_graph)
+    assert run.sparse == (density < 0.2)
+    # the device-drawn features equal the host generator's on sampled rows
+    rng = np.random.default_rng(1)
+    for r in rng.integers(0, wl.n, 4):
+        want = gs.features_bernoulli(wl.n, wl.f, density, seed=0, stream=3, row0=int(r), rows=1, binary=False)
+        np.testing.assert_array_equal(run.Xv[int(r)].cpu().numpy(), want[0])
+    rows, n_hubs = sample_rows(run.og, 400)
+    note(f"{wl.name}: {rows.size} sampled rows, {n_hubs} hub rows above {SPLIT_MIN} entries")
+    x_cols = np.unique(np.concatenate([rng.integers(0, wl.f, 120), [0, 1, wl.f - 2, wl.f - 1]])).astype(np.int64)
+    check_run(G, orc, run, rows, wl.name, x_cols=x_cols)
+    del run
+    torch.cuda.empty_cache()

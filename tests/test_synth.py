@@ -49,3 +49,15 @@ def test_feature_statistics():
     assert abs(N.mean()) < 0.01 and abs(N.std() - 1) < 0.01
     y = gs.labels(10000, 7)
     assert y.min() == 0 and y.max() == 6
+
+
+def test_c_edge_sampler_equals_numpy_loop():
+    """The C sampler draws the same pairs as the numpy loop, including graphs dense enough
+    that the first batch leaves pairs missing (several batches)."""
+    if gs.host_lib() is None:
+        gs.build_host()
+    for n, e in [(3000, 20000), (2000, 500000), (300, 40000), (50000, 400000), (10, 45)]:
+        a = gs.chung_lu(n, e, use_c=False)
+        b = gs.chung_lu(n, e)
+        np.testing.assert_array_equal(a[0], b[0])
+        np.testing.assert_array_equal(a[1], b[1])
