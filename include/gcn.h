@@ -357,6 +357,22 @@ gcn_status gcn_gemm(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_
                     size_t* ws_bytes, hipStream_t stream);
 
 /*
+ * gcn_gemm_static -- gcn_gemm for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * arguments, kernels and results as gcn_gemm, with the product's scratch (split-k partial
+ * tiles, the split weight planes of the row-panel product) taken from a static device
+ * array of GCN_STATIC_WS_BYTES that the library holds on each device it runs on, instead
+ * of from a caller workspace.  Allocates nothing.  GCN_E_CAPACITY (nothing launched) when
+ * the product needs more scratch than that; gcn_gemm's size query gives the need.  All
+ * calls on one device share its array: calls that overlap on one device (several streams
+ * or threads) race and must be serialised by the caller.  Asynchronous.
+ */
+#define GCN_STATIC_WS_BYTES (64ll << 20)
+gcn_status gcn_gemm_static(int32_t op, int64_t m, int64_t n, int64_t k, const float* d_A, int64_t lda,
+                           const float* d_B, int64_t ldb, float* d_C, int64_t ldc, const float* d_bias,
+                           int32_t epi, const float* d_mask, int64_t ldmask, hipStream_t stream);
+
+/*
  * gcn_spmm -- C[i,:] = sum_e val[e] B[idx[e],:] over compressed rows
  * i < nrows (Section IV-B backend-specialised primitives: X_csr W forward,
  * X^T G from X_csc backward).  Asynchronous.  d_ptr: nrows + 1 int64;

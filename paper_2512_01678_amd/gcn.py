@@ -102,6 +102,7 @@ _SIG = {
     "gcn_aggregate_max_bwd": (i32, [C.POINTER(gcn_graph), i32, P, i64, P, i64, P, i64, P, i64, P, C.POINTER(sz),
                                     P]),
     "gcn_gemm": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P, C.POINTER(sz), P]),
+    "gcn_gemm_static": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P]),
     "gcn_spmm": (i32, [i64, i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_spmm_xt": (i32, [i32, i32, i64, P, P, P, C.POINTER(gcn_split), P, i64, i32, P, i64, P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
@@ -317,6 +318,23 @@ def gemm(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, ws: _Workspace | Non
     _run_ws(_lib.gcn_gemm, (op, m, n, k, _ptr(A), _ld(A), _ptr(B), _ld(B), _ptr(out), _ld(out),
                             _ptr(bias), epi, _ptr(mask), _ld(mask) if mask is not None else 0),
             (P(_stream(stream)),), "gcn_gemm", ws, out.device)
+    return out
+
+
+def gemm_static(op, A, B, out, bias=None, epi=EPI_NONE, mask=None, stream=None):
+    """gcn_gemm_static: gemm with the library's static device scratch (no workspace)."""
+    if op == OP_NN:
+        m, k = A.shape
+        n = B.shape[1]
+    elif op == OP_NT:
+        m, k = A.shape
+        n = B.shape[0]
+    else:
+        k, m = A.shape
+        n = B.shape[1]
+    _check(_lib.gcn_gemm_static(op, m, n, k, _ptr(A), _ld(A), _ptr(B), _ld(B), _ptr(out), _ld(out), _ptr(bias),
+                                epi, _ptr(mask), _ld(mask) if mask is not None else 0, P(_stream(stream))),
+           "gcn_gemm_static")
     return out
 
 

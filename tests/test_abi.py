@@ -286,3 +286,19 @@ def test_epoch_memory_scales_with_nodes(G):
     a, b = _epoch_ws(G, 1_000_000, 50_000_000, w), _epoch_ws(G, 2_000_000, 50_000_000, w)
     c = _epoch_ws(G, 4_000_000, 50_000_000, w)
     assert (c - b) == pytest.approx(2 * (b - a), rel=0.02)
+
+
+def test_gemm_static_checks_before_any_device_call(G):
+    """gcn_gemm_static validates like gcn_gemm and rejects a product whose scratch exceeds the
+    static array, both before touching a device."""
+    L = G.raw_lib()
+    assert L.gcn_gemm_static(9, 4, 4, 4, 1, 4, 1, 4, 1, 4, None, 0, None, 0, None) == G.E_INVALID
+    assert L.gcn_gemm_static(G.OP_NN, 4, 4, 8, 1, 4, 1, 4, 1, 4, None, 0, None, 0, None) == G.E_INVALID
+    # the row-panel product with a long k: its split weight planes (6 k n bytes) exceed 64 MiB
+    m, n, k = 32768, 256, 50000
+    nb = G.sz(0)
+    assert L.gcn_gemm(G.OP_NN, m, n, k, None, k, None, n, None, n, None, 0, None, 0, None,
+                      C.byref(nb), None) == G.OK
+    assert nb.value > (64 << 20)
+    assert L.gcn_gemm_static(G.OP_NN, m, n, k, 256, k, 256, n, 256, n, None, 0, None, 0, None) == G.E_CAPACITY
+    assert "scratch" in L.gcn_last_error().decode()
