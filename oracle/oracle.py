@@ -400,6 +400,60 @@ def epoch(g: Graph, X, y, Ws, bs, mW, vW, mb, vb, t: int, sparse: SparseX | None
                 vW=nvW, mb=nmb, vb=nvb, aux=aux)
 
 
+def epoch_row_blocks(g: Graph, x_rows, f: int, y, Ws, bs, mW, vW, mb, vb, t: int, sparse: bool = False,
+                     block_rows: int = 65536, lr=0.01, b1=0.9, b2=0.999, eps=1e-8):
+    """``epoch`` for input features too large to hold whole (GCN aggregator, ReLU hidden layers).
+
+    x_rows(r0, r1) returns rows r0 .. r1-1 of X (fp32).  The two products that read X,
+    X W_0 in the forward pass and dW_0 = X^T Q_0 in the backward pass, run over row blocks
+    (dW_0 as the sum of the blocks' X_b^T Q_0[b], in block order); with ``sparse`` each block
+    goes through DenseToCSR / DenseToCSC and the sparse products of Algorithm 1.  Every
+    other step is the one ``epoch`` takes.  Returns loss, gradients and updated parameters.
+    """
+    n = g.n
+    L = len(Ws)
+    Wd = [np.asarray(w, np.float64) for w in Ws]
+    blocks = [(r0, min(n, r0 + block_rows)) for r0 in range(0, n, block_rows)]
+    M0 = np.zeros((n, Wd[0].shape[1]))
+    for r0, r1 in blocks:
+        Xb = np.asarray(x_rows(r0, r1), np.float32)
+        if sparse:
+            rp, col, val = dense_to_csr(Xb)
+            M0[r0:r1] = spmm(rp, col, val, Wd[0])
+        else:
+            M0[r0:r1] = matmul(Xb, Wd[0])
+    Zs = [aggregate(g, M0, bs[0])]
+    Hs = [None]
+    for l in range(1, L):
+        Hs.append(np.maximum(Zs[-1], 0.0))
+        Zs.append(aggregate(g, matmul(Hs[l], Wd[l]), bs[l]))
+    loss, G, _ = softmax_ce(Zs[-1], y)
+    dWs, dbs = [None] * L, [None] * L
+    for l in range(L - 1, -1, -1):
+        dbs[l] = G.sum(axis=0)
+        Q = aggregate(g, G)
+        if l > 0:
+            dWs[l] = matmul(Hs[l].T, Q)
+            G = matmul(Q, Wd[l].T) * (Zs[l - 1] > 0.0)
+            continue
+        dW0 = np.zeros_like(Wd[0])
+        for r0, r1 in blocks:
+            Xb = np.asarray(x_rows(r0, r1), np.float32)
+            if sparse:
+                cp, row, val = dense_to_csc(Xb)
+                dW0 += spmm(cp, row, val, Q[r0:r1])
+            else:
+                dW0 += matmul(Xb.T, Q[r0:r1])
+        dWs[0] = dW0
+    out = dict(loss=loss, dWs=dWs, dbs=dbs, Ws=[], bs=[], mW=[], vW=[], mb=[], vb=[])
+    for l in range(L):
+        a, m_, v_ = adam(Ws[l], dWs[l], mW[l], vW[l], t, lr, b1, b2, eps)
+        out["Ws"].append(a), out["mW"].append(m_), out["vW"].append(v_)
+        a, m_, v_ = adam(bs[l], dbs[l], mb[l], vb[l], t, lr, b1, b2, eps)
+        out["bs"].append(a), out["mb"].append(m_), out["vb"].append(v_)
+    return out
+
+
 def dense_operator(g: Graph, kind: str = "gcn") -> np.ndarray:
     """The aggregation operator (A_hat by default) as a dense fp64 matrix (small graphs only)."""
     A = np.zeros((g.n, g.n), np.float64)

@@ -448,6 +448,25 @@ def test_sparse_path_equals_dense_path(orc):
         np.testing.assert_allclose(a, b, atol=1e-14)
 
 
+@pytest.mark.parametrize("sparse", [False, True])
+@pytest.mark.parametrize("widths", [(30, 8, 4), (20, 7, 6, 3)])
+def test_row_block_epoch_equals_epoch(orc, sparse, widths):
+    """The row-block epoch (for features too large to hold) against the whole-matrix epoch:
+    same loss, gradients and Adam step, with blocks that do not divide n."""
+    n = 40
+    src, dst, X, Ws, bs, y = tiny_problem(23, n=n, widths=widths, density=0.1)
+    g = orc.build_csr(n, src, dst)
+    z = [np.zeros_like(w) for w in Ws]
+    zb = [np.zeros_like(b) for b in bs]
+    want = orc.epoch(g, X, y, Ws, bs, z, z, zb, zb, 1, sparse=orc.SparseX(X) if sparse else None)
+    got = orc.epoch_row_blocks(g, lambda r0, r1: X[r0:r1], X.shape[1], y, Ws, bs, z, z, zb, zb, 1,
+                               sparse=sparse, block_rows=7)
+    assert got["loss"] == pytest.approx(want["loss"], rel=1e-14)
+    for k in ("dWs", "dbs", "Ws", "bs"):
+        for a, b in zip(got[k], want[k]):
+            np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-15)
+
+
 def test_epochs_match_torch_training(orc):
     """Three oracle epochs against torch autograd + torch.optim.Adam on a dense A_hat."""
     src, dst, X, Ws, bs, y = tiny_problem(31, n=25, widths=(5, 6, 3))
