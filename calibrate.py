@@ -79,9 +79,8 @@ def main():
             nnz = sx.nnz
             dense_f = timed(lambda: G.gemm(G.OP_NN, X, W, out, ws=ws), args.reps)
             dense_b = timed(lambda: G.gemm(G.OP_TN, X, Q, dW, ws=ws), args.reps)
-            sparse_f = timed(lambda: G.spmm(sx.row_ptr, sx.col[:nnz], sx.val[:nnz], W, out), args.reps)
-            # the backward product in the form layer 0's backward takes (tiled by row chunks
-            # where the columns are long enough)
+            # both sparse products in the form layer 0 takes them
+            sparse_f = timed(lambda: G.spmm_xw(sx, W, out), args.reps)
             sparse_b = timed(lambda: G.spmm_xt(sx, Q, dW), args.reps)
             dflop, sflop = 2.0 * n * F * f1, 2.0 * nnz * f1
             r = {"F": F, "density": nnz / (n * F), "nnz": nnz,

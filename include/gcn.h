@@ -404,6 +404,19 @@ gcn_status gcn_spmm_xt(int32_t n, int32_t f, int64_t nnz, const int64_t* d_col_p
                        int32_t w, float* d_C, int64_t ldc, void* d_ws, size_t* ws_bytes, hipStream_t stream);
 
 /*
+ * gcn_spmm_xw -- C = X W with X (n x f) in its CSR view: the forward SpMM of a sparse
+ * first layer (Algorithm 1, Forward; the product gcn_layer_fwd takes).  Asynchronous.
+ * d_row_ptr: n + 1 int64; d_col, d_val: nnz column indices (ascending within a row,
+ * 0 <= col < f) and values, as gcn_feature_stats writes them; d_W: f x w (pitch ldw);
+ * d_C: n x w (pitch ldc), overwritten.  Lane slices of each row gather a row of W per
+ * entry, as the aggregation does (W of the layer stays in L2).  Deterministic.  Needs no
+ * workspace (the size query returns 0).
+ */
+gcn_status gcn_spmm_xw(int32_t n, int32_t f, int64_t nnz, const int64_t* d_row_ptr, const int32_t* d_col,
+                       const float* d_val, const float* d_W, int64_t ldw, int32_t w, float* d_C, int64_t ldc,
+                       void* d_ws, size_t* ws_bytes, hipStream_t stream);
+
+/*
  * gcn_column_sums -- out[c] = sum_i G[i,c] (the bias gradient) and, when
  * d_row_vals != NULL, *d_mean = (1/rows) sum_i row_vals[i].  Fixed summation
  * order.  Asynchronous.

@@ -283,19 +283,7 @@ gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, c
   if (bits_written) *bits_written = want_bits;  // the aggregation epilogue writes them
   if (!run) return GCN_OK;
   if (x) {
-    AggParams p{};
-    p.n = n;
-    p.row_ptr = x->row_ptr;
-    p.col = x->col;
-    p.val = x->val;
-    p.M = W;
-    p.ldm = L->f_out;
-    p.w = L->f_out;
-    p.Z = M;
-    p.ldz = ldm;
-    p.epi = AGG_NONE;
-    p.tag = "spmm_xw";
-    GCN_TRY(launch_aggregate(p, x->nnz, nullptr, nullptr, s));
+    GCN_TRY(launch_spmm_xw(n, x->nnz, x->row_ptr, x->col, x->val, W, L->f_out, L->f_out, M, ldm, s));
   } else {
     GCN_TRY(launch_gemm(with_split(q, sj, nsj), gws, s));
   }
@@ -799,6 +787,20 @@ gcn_status gcn_spmm_xt(int32_t n, int32_t f, int64_t nnz, const int64_t* d_col_p
     return fail(GCN_E_INVALID, "gcn_spmm_xt: NULL argument");
   if (f == 0 || w == 0) return GCN_OK;
   return launch_spmm_xt(n, f, nnz, d_col_ptr, d_row, d_cval, csc_split, d_B, ldb, w, d_C, ldc, d_ws, stream);
+}
+
+gcn_status gcn_spmm_xw(int32_t n, int32_t f, int64_t nnz, const int64_t* d_row_ptr, const int32_t* d_col,
+                       const float* d_val, const float* d_W, int64_t ldw, int32_t w, float* d_C, int64_t ldc,
+                       void* d_ws, size_t* ws_bytes, hipStream_t stream) {
+  g_err.clear();
+  if (n < 0 || f < 0 || nnz < 0 || w < 0 || ldw < w || ldc < w) return fail(GCN_E_INVALID, "gcn_spmm_xw: bad size or pitch");
+  bool query = false;
+  GCN_TRY(ws_protocol(d_ws, ws_bytes, 0, "gcn_spmm_xw", &query));
+  if (query) return GCN_OK;
+  if (n > 0 && w > 0 && (!d_row_ptr || (nnz > 0 && (!d_col || !d_val || !d_W)) || !d_C))
+    return fail(GCN_E_INVALID, "gcn_spmm_xw: NULL argument");
+  if (n == 0 || w == 0) return GCN_OK;
+  return launch_spmm_xw(n, nnz, d_row_ptr, d_col, d_val, d_W, ldw, w, d_C, ldc, stream);
 }
 
 gcn_status gcn_column_sums(int64_t rows, int32_t w, const float* d_G, int64_t ldg, float* d_out,

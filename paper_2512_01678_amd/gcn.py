@@ -105,6 +105,7 @@ _SIG = {
     "gcn_gemm_static": (i32, [i32, i64, i64, i64, P, i64, P, i64, P, i64, P, i32, P, i64, P]),
     "gcn_spmm": (i32, [i64, i64, P, P, P, i64, i32, P, i64, P, i64, C.POINTER(gcn_split), P, C.POINTER(sz), P]),
     "gcn_spmm_xt": (i32, [i32, i32, i64, P, P, P, C.POINTER(gcn_split), P, i64, i32, P, i64, P, C.POINTER(sz), P]),
+    "gcn_spmm_xw": (i32, [i32, i32, i64, P, P, P, P, i64, i32, P, i64, P, C.POINTER(sz), P]),
     "gcn_column_sums": (i32, [i64, i32, P, i64, P, P, P, P, C.POINTER(sz), P]),
     "gcn_adam": (i32, [C.POINTER(gcn_adam_tensor), i32, i32, f64, f64, f64, f64, P]),
     "gcn_adam_device_step": (i32, [C.POINTER(gcn_adam_tensor), i32, P, f64, f64, f64, f64, P]),
@@ -352,6 +353,15 @@ def spmm_xt(sx: "SparseFeatures", B: torch.Tensor, out: torch.Tensor, stream=Non
     c = sx.c
     _run_ws(_lib.gcn_spmm_xt, (c.n, c.f, c.nnz, c.col_ptr, c.row, c.cval, C.byref(c.csc_split), _ptr(B), _ld(B), w,
                                _ptr(out), _ld(out)), (P(_stream(stream)),), "gcn_spmm_xt", None, out.device)
+    return out
+
+
+def spmm_xw(sx: "SparseFeatures", W: torch.Tensor, out: torch.Tensor, stream=None):
+    """out (n x w) = X W from the CSR view of sparse features sx (Algorithm 1, Forward)."""
+    f, w = W.shape
+    c = sx.c
+    _run_ws(_lib.gcn_spmm_xw, (c.n, c.f, c.nnz, c.row_ptr, c.col, c.val, _ptr(W), _ld(W), w, _ptr(out), _ld(out)),
+            (P(_stream(stream)),), "gcn_spmm_xw", None, out.device)
     return out
 
 

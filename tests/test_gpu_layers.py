@@ -251,6 +251,43 @@ def test_spmm_xt_chunk_edges(G, orc, case, monkeypatch):
         assert np.all(got[np.abs(X).sum(0) == 0] == 0.0)  # empty columns give exact zeros
 
 
+@pytest.mark.parametrize("w", [128, 100, 37, 16, 8])
+def test_sparse_forward_product_shapes(G, orc, w):
+    """The forward X_csr W of a sparse first layer (no edges, so the layer output is X W + b),
+    in gcn_layer_fwd and through gcn_spmm_xw: 5000 features, empty rows, rows with every
+    feature nonzero, a band of features no row touches, widths with and without 16-byte
+    rows; against the fp64 product."""
+    xw = "gather"
+    n, F = 1000, 5000
+    rng = np.random.default_rng(31 + w)
+    X = np.where(rng.random((n, F)) < 0.1, rng.standard_normal((n, F)), 0.0).astype(np.float32)
+    X[:, 4096 + 64:4096 + 128] = 0.0
+    X[7] = 0.0
+    X[500] = rng.standard_normal(F).astype(np.float32)
+    X[999, :4096] = 1.0
+    dg = G.build_csr(n, dev(np.zeros(0, np.int32)), dev(np.zeros(0, np.int32)))
+    info, sx = G.feature_stats(dev(X))
+    assert info["mode"] == G.SPARSE
+    W0 = rng.standard_normal((F, w)).astype(np.float32)
+    b0 = rng.standard_normal(w).astype(np.float32)
+    L = G.make_layer(F, w, F, G.pitch(w), G.ACT_NONE, 0)
+    out = G.padded(n, w)
+    G.layer_fwd(dg, L, None, sx, dev(W0), dev(b0), out)
+    ref = orc.matmul(X, W0) + b0
+    mag = orc.matmul(np.abs(X), np.abs(W0)) + np.abs(b0)
+    got = host(out)
+    assert_mag_close(got, ref, mag, f"X_csr W ({xw}, w = {w})")
+    np.testing.assert_array_equal(got[7], b0)  # an empty row is the bias exactly
+    again = G.padded(n, w)
+    G.layer_fwd(dg, L, None, sx, dev(W0), dev(b0), again)
+    np.testing.assert_array_equal(host(again), got)  # fixed order
+    # the same product through its own entry point (no bias)
+    C2 = torch.full((n, w), float("nan"), device="cuda")
+    G.spmm_xw(sx, dev(W0), C2)
+    assert_mag_close(host(C2), orc.matmul(X, W0), orc.matmul(np.abs(X), np.abs(W0)), f"gcn_spmm_xw ({xw}, w = {w})")
+    assert np.all(host(C2)[7] == 0.0)
+
+
 # ---------------------------------------------------------------------------
 # whole epochs (end-to-end parity, determinism)
 # ---------------------------------------------------------------------------
