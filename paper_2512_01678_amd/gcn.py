@@ -250,7 +250,15 @@ class SparseFeatures:
         return self.c.nnz
 
 
-def feature_stats(X: torch.Tensor, tau=(4, 5), force_mode=-1, materialize=None, csc=True,
+# The sparse-path threshold tau measured on MI355X (Section IV-B: tau = 1 - gamma, gamma the
+# sparse product's useful-work efficiency relative to the dense one): the training step's
+# dense and sparse forms of the input-feature products cross at about 6.25 % density on
+# this GPU (2^21 rows, 1024 and 4096 features, width 128), so tau = 15/16.  The paper's
+# testbed gave about 0.8 (pass tau=(4, 5) for that).
+TAU_MI355X = (15, 16)
+
+
+def feature_stats(X: torch.Tensor, tau=TAU_MI355X, force_mode=-1, materialize=None, csc=True,
                   row_nnz: torch.Tensor | None = None, stream=None):
     """Density probe (+ X_csr / X_csc when materialize is True, or None -> by mode).
 

@@ -1,9 +1,10 @@
 """Parity at the full size of every workload, in the benchmark's launch configuration.
 
 One training epoch (Algorithm 1 forward and backward, the softmax cross-entropy, Adam)
-of each full-size workload runs on the GPU exactly as bench.py runs it: X at the
-bench's pitch, the density probe with tau = 4/5 choosing the path, the CSC view for a
-sparse first layer, every product at its automatic kernel choice.  Then the fp64 oracle
+of each full-size workload runs on the GPU as bench.py runs it: X at the bench's pitch,
+the density probe choosing the path (with the paper's tau = 4/5, so that the RMAT
+features at 10 % density take the sparse path too), the CSC view for a sparse first
+layer, every product at its automatic kernel choice.  Then the fp64 oracle
 checks, from the GPU's own layer inputs (unit parity, each element against its
 magnitude scale sum |terms|):
   * every hidden layer's output H_{l+1} (and the saved aggregate of an aggregate-first

@@ -125,7 +125,7 @@ def test_feature_stats_bit_exact(G, orc, case):
     mode = orc.sparse_decision(nnz, n, f)
     Xd = pitched(X, G.pitch(f) + 4)
     rnd = torch.zeros(n, dtype=torch.int64, device="cuda")
-    info, sx = G.feature_stats(Xd, materialize=True, row_nnz=rnd)
+    info, sx = G.feature_stats(Xd, tau=(4, 5), materialize=True, row_nnz=rnd)
     assert info["nnz"] == nnz and info["mode"] == mode
     assert info["sparsity"] == pytest.approx(orc.sparsity(nnz, n, f), abs=1e-15)
     np.testing.assert_array_equal(host(rnd), rn)
@@ -142,12 +142,21 @@ def test_feature_stats_bit_exact(G, orc, case):
 def test_feature_decision_tau_and_force(G, orc):
     X = np.zeros((40, 25), np.float32)
     X.flat[: 40 * 25 // 5 + 1] = 1.0
-    info, _ = G.feature_stats(dev(X), materialize=False)
+    info, _ = G.feature_stats(dev(X), tau=(4, 5), materialize=False)
     assert info["mode"] == G.DENSE
     info, _ = G.feature_stats(dev(X), tau=(3, 4), materialize=False)
     assert info["mode"] == G.SPARSE
     info, _ = G.feature_stats(dev(X), force_mode=G.SPARSE, materialize=False)
     assert info["mode"] == G.SPARSE
+    # the default threshold, measured on this GPU: tau = 15/16, sparse iff nnz <= N F / 16
+    assert G.TAU_MI355X == (15, 16)
+    Y = np.zeros((64, 50), np.float32)
+    Y.flat[: 64 * 50 // 16] = 2.0
+    info, _ = G.feature_stats(dev(Y), materialize=False)
+    assert info["mode"] == G.SPARSE and orc.sparse_decision(info["nnz"], 64, 50, 15, 16) == G.SPARSE
+    Y.flat[64 * 50 // 16] = 2.0
+    info, _ = G.feature_stats(dev(Y), materialize=False)
+    assert info["mode"] == G.DENSE and orc.sparse_decision(info["nnz"], 64, 50, 15, 16) == G.DENSE
 
 
 # ---------------------------------------------------------------------------

@@ -168,7 +168,7 @@ def test_layer_sparse_input(G, orc, cora, xt, monkeypatch):
     monkeypatch.setenv("GCN_XT", xt)
     og, dg, n = cora.og, cora.dg, cora.wl.n
     X, W0, b0 = cora.X, cora.Ws[0], cora.bs[0] + 0.05
-    info, sx = G.feature_stats(dev(X))
+    info, sx = G.feature_stats(dev(X), tau=(4, 5))
     assert info["mode"] == G.SPARSE
     L = G.make_layer(1433, 16, 1433, G.pitch(16), G.ACT_RELU, 0)
     out = G.padded(n, 16)
@@ -197,7 +197,7 @@ def test_sparse_weight_gradient_row_chunks(G, orc, w, monkeypatch):
     X[:, 5] = 0.0
     X[:, 9] = rng.standard_normal(n).astype(np.float32)
     dg = G.build_csr(n, dev(np.zeros(0, np.int32)), dev(np.zeros(0, np.int32)))
-    info, sx = G.feature_stats(dev(X))
+    info, sx = G.feature_stats(dev(X), tau=(4, 5))
     assert info["mode"] == G.SPARSE
     L = G.make_layer(F, w, F, G.pitch(w), G.ACT_RELU, 0)
     Gr = (rng.standard_normal((n, w)) / n).astype(np.float32)
@@ -237,7 +237,7 @@ def test_spmm_xt_chunk_edges(G, orc, case, monkeypatch):
         X[0, ::10] = 1.5
     if case == "no_entries":
         X[:] = 0.0
-    info, sx = G.feature_stats(dev(X))
+    info, sx = G.feature_stats(dev(X), tau=(4, 5))
     assert info["mode"] == G.SPARSE and info["nnz"] == np.count_nonzero(X)
     Q = rng.standard_normal((n, w)).astype(np.float32)
     ref = orc.matmul(X.T, Q)
@@ -266,7 +266,7 @@ def test_sparse_forward_product_shapes(G, orc, w):
     X[500] = rng.standard_normal(F).astype(np.float32)
     X[999, :4096] = 1.0
     dg = G.build_csr(n, dev(np.zeros(0, np.int32)), dev(np.zeros(0, np.int32)))
-    info, sx = G.feature_stats(dev(X))
+    info, sx = G.feature_stats(dev(X), tau=(4, 5))
     assert info["mode"] == G.SPARSE
     W0 = rng.standard_normal((F, w)).astype(np.float32)
     b0 = rng.standard_normal(w).astype(np.float32)
@@ -590,7 +590,7 @@ def test_epoch_rmat_4096_features_sparse(G, orc, xt, monkeypatch):
     device.bernoulli_into(Xd, 0.1, seed=0, stream=3)
     X = gs.features_bernoulli(n, 4096, 0.1, seed=0, stream=3, binary=False)
     np.testing.assert_array_equal(host(Xd).astype(np.float32), X)
-    info, sx = G.feature_stats(Xd)
+    info, sx = G.feature_stats(Xd, tau=(4, 5))
     assert info["mode"] == G.SPARSE
     p = Problem.__new__(Problem)
     p.wl, p.og, p.dg = wl, orc.build_csr(n, s, d), G.build_csr(n, dev(s), dev(d))
@@ -611,7 +611,7 @@ def test_epoch_rmat_4096_features_densities(G, orc, density):
     Xd = torch.zeros((n, 4096), device="cuda")
     device.bernoulli_into(Xd, density, seed=0, stream=3)
     X = gs.features_bernoulli(n, 4096, density, seed=0, stream=3, binary=False)
-    info, sx = G.feature_stats(Xd)
+    info, sx = G.feature_stats(Xd, tau=(4, 5))
     assert info["nnz"] == np.count_nonzero(X)
     sparse = density < 0.2
     assert info["mode"] == (G.SPARSE if sparse else G.DENSE)
