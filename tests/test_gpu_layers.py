@@ -337,7 +337,7 @@ def run_epochs(G, orc, p, epochs, sparse, aggs=None, csc=True):
     Xd = dev(p.X)
     sx = None
     if sparse:
-        info, sx = G.feature_stats(Xd, csc=csc)
+        info, sx = G.feature_stats(Xd, tau=(4, 5), csc=csc)
         assert info["mode"] == G.SPARSE
     m = G.Model(n, p.wl.widths, p.Ws, p.bs, x_sparse=sparse, ld_x=p.wl.f,
                 aggs=[AGGS[a] for a in aggs] if aggs else None)
