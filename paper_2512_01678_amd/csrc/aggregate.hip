@@ -515,23 +515,6 @@ gcn_status launch_spmm_xt(int64_t n, int32_t F, int64_t nnz, const int64_t* col_
   return launch_aggregate(p, nnz, csc_split, ws, s);
 }
 
-gcn_status launch_spmm_xw(int64_t n, int64_t nnz, const int64_t* row_ptr, const int32_t* col, const float* val,
-                          const float* W, int64_t ldw, int32_t w, float* C, int64_t ldc, hipStream_t s) {
-  AggParams p{};
-  p.n = (int32_t)n;
-  p.row_ptr = row_ptr;
-  p.col = col;
-  p.val = val;
-  p.M = W;
-  p.ldm = ldw;
-  p.w = w;
-  p.Z = C;
-  p.ldz = ldc;
-  p.epi = AGG_NONE;
-  p.tag = "spmm_xw";
-  return launch_aggregate(p, nnz, nullptr, nullptr, s);
-}
-
 gcn_status launch_spmm_t_atomic(int64_t nrows, const int64_t* ptr, const int32_t* idx, const float* val,
                                 const float* B, int64_t ldb, int32_t w, int64_t out_rows, float* C, int64_t ldc,
                                 int64_t nnz, hipStream_t s) {

@@ -184,6 +184,25 @@ gcn_status loss_pass(int32_t n, const gcn_layer* L, const float* G, const float*
   return launch_colsum(n, 0, nullptr, 0, nullptr, row_loss, loss, cws, s);
 }
 
+// X_csr W of a sparse first layer: lane slices of each row gather a row of W per entry
+// (the aggregation kernel with the stored values of X).
+gcn_status launch_spmm_xw(int64_t n, int64_t nnz, const int64_t* row_ptr, const int32_t* col, const float* val,
+                          const float* W, int64_t ldw, int32_t w, float* C, int64_t ldc, hipStream_t s) {
+  AggParams p{};
+  p.n = (int32_t)n;
+  p.row_ptr = row_ptr;
+  p.col = col;
+  p.val = val;
+  p.M = W;
+  p.ldm = ldw;
+  p.w = w;
+  p.Z = C;
+  p.ldz = ldc;
+  p.epi = AGG_NONE;
+  p.tag = "spmm_xw";
+  return launch_aggregate(p, nnz, nullptr, nullptr, s);
+}
+
 gcn_status layer_fwd(const gcn_graph* g, const gcn_layer* L, const float* Hin, const gcn_sparse_x* x,
                      const float* W, const float* b, float* Hout, float* saved, const int32_t* labels,
                      float* loss, float* logits, Arena& a, hipStream_t s, uint32_t* relu_bits = nullptr,

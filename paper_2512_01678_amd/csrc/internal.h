@@ -132,9 +132,6 @@ size_t xt_tiled_workspace(int64_t n, int32_t F, int32_t w);
 gcn_status launch_spmm_xt_tiled(int64_t n, int32_t F, const int64_t* col_ptr, const int32_t* row, const float* cval,
                                 int64_t nnz, const float* B, int64_t ldb, int32_t w, float* C, int64_t ldc, void* ws,
                                 hipStream_t s);
-// X_csr W (n x w) of a sparse first layer (gcn_spmm_xw): a row of W gathered per entry.
-gcn_status launch_spmm_xw(int64_t n, int64_t nnz, const int64_t* row_ptr, const int32_t* col, const float* val,
-                          const float* W, int64_t ldw, int32_t w, float* C, int64_t ldc, hipStream_t s);
 // X^T B from the CSC view in the form xt_tiled_enabled picks (gcn_spmm_xt).
 size_t spmm_xt_workspace(int64_t n, int32_t F, int64_t nnz, int32_t w, const gcn_split* csc_split);
 gcn_status launch_spmm_xt(int64_t n, int32_t F, int64_t nnz, const int64_t* col_ptr, const int32_t* row,
