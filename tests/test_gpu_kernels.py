@@ -200,6 +200,33 @@ def test_aggregate_widths(G, orc, agg_graph, w, vec):
         assert torch.isnan(Zd.as_strided((n, ld), (ld, 1))[:, w:]).all()
 
 
+@pytest.fixture(scope="module")
+def dense_rows_graph(G, orc):
+    """Mean degree about 90: slices of 16 and 32 lanes take more than 8 entries of an
+    average row, so the aggregation keeps 16 neighbour loads in flight per lane."""
+    s, d = gs.chung_lu(2000, 90000, seed=4)
+    return orc.build_csr(2000, s, d), G.build_csr(2000, dev(s), dev(d))
+
+
+@pytest.mark.parametrize("w", [33, 40, 47, 64, 65, 100, 128])
+def test_aggregate_widths_long_rows(G, orc, dense_rows_graph, w):
+    og, dg = dense_rows_graph
+    assert og.nnz / og.n > 64
+    rng = np.random.default_rng(100 + w)
+    n = og.n
+    M = rng.standard_normal((n, w)).astype(np.float32)
+    b = rng.standard_normal(w).astype(np.float32)
+    ld = G.pitch(w)
+    Md = pitched(M, ld)
+    Zd = pitched(np.zeros((n, w), np.float32), ld)
+    mask = rng.standard_normal((n, w)).astype(np.float32)
+    Z, mag = orc.aggregate(og, M, b, want_mag=True)
+    for epi in (G.EPI_NONE, G.EPI_RELU, G.EPI_MASK):
+        G.aggregate(dg, Md, Zd, bias=dev(b), epi=epi, mask=pitched(mask, ld) if epi == G.EPI_MASK else None)
+        want = Z if epi == G.EPI_NONE else (np.maximum(Z, 0) if epi == G.EPI_RELU else Z * (mask > 0))
+        assert_mag_close(host(Zd), want, mag, f"aggregate long rows w={w} epi={epi}")
+
+
 def test_aggregate_no_bias_deterministic(G, orc, agg_graph):
     og, dg = agg_graph
     M = np.random.default_rng(0).standard_normal((og.n, 256)).astype(np.float32)
