@@ -559,8 +559,15 @@ gcn_status launch_aggregate(const AggParams& p, int64_t nnz, const gcn_split* sp
   const bool vec4 = use_vec4(p);
   const int vec = vec4 ? 4 : 1;
   int need = (int)ceil_div(p.w, vec);
+  // A slice spans at most 32 lanes (128 columns with 16-byte loads); wider rows take
+  // several column groups (blockIdx.y), which are dispatched one after the other, so a
+  // 256-wide aggregation gathers 512-byte half rows in two passes.  The 32-lane kernel
+  // holds 71 VGPRs (7 wavefronts per SIMD) against 112 (4) for a 64-lane slice, and runs
+  // 256-wide rows about 10 % faster.  The softmax epilogue needs the whole row in one
+  // slice, so it keeps up to 64 lanes.
+  const int max_lanes = p.epi == AGG_SOFTMAX ? 64 : 32;
   int lanes = 1;
-  while (lanes < need && lanes < 64) lanes <<= 1;
+  while (lanes < need && lanes < max_lanes) lanes <<= 1;
   if (p.epi == AGG_SOFTMAX && need > lanes)
     return fail(GCN_E_UNSUPPORTED, "softmax epilogue needs width <= 256 (vector) or 64 (scalar)");
   if (has_split(split) && !ws) return fail(GCN_E_INVALID, "aggregation of split rows needs a workspace");
