@@ -71,7 +71,8 @@ def abs_agg(orc, og, A):
 @pytest.mark.parametrize("order", ["TF", "AF"])
 @pytest.mark.parametrize("fi,fo,act", [(128, 256, "relu"), (256, 40, "softmax"), (100, 256, "relu"),
                                        (41, 47, "none"), (256, 7, "softmax"), (602, 256, "relu"),
-                                       (64, 300, "relu"), (33, 5, "none"), (120, 520, "relu")])
+                                       (64, 300, "relu"), (33, 5, "none"), (120, 520, "relu"),
+                                       (64, 128, "softmax"), (256, 200, "softmax")])
 def test_layer_forward(G, orc, small, order, fi, fo, act):
     if order == "AF" and act == "softmax":
         pytest.skip("aggregate-first is never chosen for the loss layer")
