@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--tau", default="15/16",
                     help="sparse-path threshold tau as num/den (15/16: measured on MI355X; the paper's is 4/5)")
     ap.add_argument("--force-mode", default="auto", choices=["auto", "dense", "sparse"])
+    ap.add_argument("--row-order", default="auto", choices=["auto", "on", "off"],
+                    help="aggregations take the graph rows longest first (on) or in row order (off); "
+                         "auto: whichever times faster for the widest hidden layer (untimed setup)")
     ap.add_argument("--csc", default="on", choices=["on", "off"],
                     help="off: no X_csc view; the sparse backward X^T Q uses atomic adds from X_csr")
     ap.add_argument("--agg", default="gcn", choices=["gcn", "sum", "mean", "max"],
@@ -222,7 +225,9 @@ def main():
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
-    g = G.build_csr(wl.n, sd, dd)
+    g = G.build_csr(wl.n, sd, dd, order=args.row_order != "off")
+    if args.row_order == "auto":
+        G.tune_row_order(g, max(wl.widths[1:-1]) if len(wl.widths) > 2 else wl.widths[-1])
     t_csr = time.perf_counter() - t0
     tau = tuple(int(v) for v in args.tau.split("/"))
     force = {"auto": -1, "dense": G.DENSE, "sparse": G.SPARSE}[args.force_mode]
@@ -412,7 +417,7 @@ def main():
         "config": {"workload": wl.name, "nodes": wl.n, "nnz_A_plus_I": g.nnz, "widths": list(wl.widths),
                    "feature_path": "sparse" if sparse else "dense", "sparsity": round(info["sparsity"], 6),
                    "orders": ["AF" if o == G.AGGREGATE_FIRST else "TF" for o in m.orders()],
-                   "aggregator": args.agg, "x_csc": sparse and args.csc == "on",
+                   "aggregator": args.agg, "row_order": g.order is not None, "x_csc": sparse and args.csc == "on",
                    "timed_events": dominant, "hip_graph": bool(args.graph),
                    "af_layer": None if G.AGGREGATE_FIRST not in m.orders() else
                    "fused kernel" if os.environ.get("GCN_AF_FUSED") == "1" else "aggregation + GEMM",

@@ -110,6 +110,12 @@ typedef struct gcn_graph {
   float* dinv;        /* device, n */
   float* val;         /* device, nnz_cap: A_hat entries (set by gcn_build_csr) */
   gcn_split split;    /* hub rows (optional; see gcn_split) */
+  int32_t* order;     /* device, n, or NULL: the order in which the aggregations over the
+                         graph take the rows.  When non-NULL on entry to gcn_build_csr it is
+                         written: rows by decreasing length class (4 classes per power of two
+                         of the degree), ties in row order, so that the long rows start first
+                         and the short ones fill the end of each launch.  Every result is the
+                         same, bit for bit, with or without it; NULL takes rows 0 .. n-1. */
 } gcn_graph;
 
 /*
@@ -173,7 +179,8 @@ typedef struct gcn_layer {
  * pairs count once; each node gets one self-loop.  On entry g->n, g->nnz_cap
  * and the five device pointers must be set; nnz_cap = 2 n_edges + n always
  * suffices.  On return g->nnz holds the entry count.  When g->split.rows is
- * non-NULL the hub split plan is built too (g->split.order is left NULL).
+ * non-NULL the hub split plan is built too (g->split.order is left NULL); when
+ * g->order is non-NULL the row order is written (see gcn_graph).
  * Errors: GCN_E_RANGE if an endpoint is outside [0, n) (outputs undefined),
  * GCN_E_CAPACITY if nnz > nnz_cap or the workspace is short.
  */

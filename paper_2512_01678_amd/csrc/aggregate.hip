@@ -137,6 +137,8 @@ __device__ __forceinline__ void finish_row(const AggParams& p, int64_t row, cons
 // Every row whose length is at most skip_over (all rows when there is no split plan).
 // One group per row; the hardware overlaps many resident wavefronts, which hides
 // the per-row chain of dependent loads better than prefetching across rows does.
+// Group g takes row p.order[g] when the graph carries a row order (long rows first:
+// they start early and the short rows fill the end of the launch), else row g.
 template <int LANES, int VEC, int EPI>
 __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, int64_t skip_over) {
   const Lanes L = lanes_of<LANES, VEC>(slots);
@@ -152,7 +154,8 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, in
     typename Vec<VEC>::T mine = Vec<VEC>::zero();
     bool own = false;
     for (int r = 0; r < slots && row0 + r < p.n; ++r) {
-      const int64_t beg = p.row_ptr[row0 + r], end = p.row_ptr[row0 + r + 1];
+      const int64_t row = p.order ? p.order[row0 + r] : row0 + r;
+      const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
       if (end - beg > skip_over) continue;  // a long row: k_combine finishes it
       const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));
       if (L.slot == r) {
@@ -160,10 +163,11 @@ __global__ void __launch_bounds__(kBlock) k_aggregate(AggParams p, int slots, in
         own = true;
       }
     }
-    finish_row<LANES, VEC, EPI, true>(p, row0 + L.slot, mine, L, cok, own);
+    const int64_t vr = row0 + L.slot;  // this slice's row, in processing order
+    finish_row<LANES, VEC, EPI, true>(p, p.order && vr < p.n ? p.order[vr] : vr, mine, L, cok, own);
   } else {
-    const int64_t row = g;
-    if (row >= p.n) return;  // whole groups leave together
+    if (g >= p.n) return;  // whole groups leave together
+    const int64_t row = p.order ? p.order[g] : g;
     const int64_t beg = p.row_ptr[row], end = p.row_ptr[row + 1];
     if (end - beg > skip_over) return;
     const auto acc = accumulate<LANES, VEC>(p, beg, end, L, slots, cok, load_first<LANES>(p, beg, end, L));

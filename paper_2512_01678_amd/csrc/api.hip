@@ -147,6 +147,7 @@ AggParams graph_agg(const gcn_graph* g, int32_t w, const float* M, int64_t ldm, 
   p.Z = Z;
   p.ldz = ldz;
   p.epi = AGG_NONE;
+  p.order = g->order;
   return p;
 }
 

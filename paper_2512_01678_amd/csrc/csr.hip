@@ -17,6 +17,11 @@
 //  5. scan the unique counts (the degrees) into row_ptr; compact into col_idx
 //     and write dinv = (float)(1 / sqrt((double)deg)).
 //  6. write the entries of A_hat, val[e] = dinv[row] * dinv[col[e]] (fp32).
+//  7. (optional) the row order of the aggregations: rows by decreasing length class,
+//     longest first, so that the long rows start early and the short ones fill the end
+//     of a launch (a longest-job-first schedule; the results do not depend on it).  A
+//     stable counting sort over 64 classes of the degree: per-block class counts, one
+//     scan in class-major order, then each block places its rows (ties in row order).
 #include "internal.h"
 
 namespace gcn {
@@ -37,7 +42,13 @@ struct CsrWs {
   uint32_t* bitmap;   // kLargeBlocks * words
   int64_t words;
   void* split;        // hub split plan scratch
+  int32_t* ord_cnt;   // kClasses * blocks of 256 rows: rows per (class, block)
+  int64_t* ord_off;   // kClasses * blocks + 1: their exclusive scan
 };
+
+constexpr int kClasses = 64;
+constexpr int kOrderBlock = 256;
+inline int64_t order_blocks(int32_t n) { return ceil_div(n > 0 ? n : 1, kOrderBlock); }
 
 CsrWs carve(Arena& a, int32_t n, int64_t n_edges) {
   CsrWs w;
@@ -47,10 +58,13 @@ CsrWs carve(Arena& a, int32_t n, int64_t n_edges) {
   w.raw = a.take<int32_t>(2 * n_edges + n);
   w.lists = a.take<int32_t>(3 * (int64_t)n);
   w.flags = a.take<int32_t>(8);
-  w.scan = a.take<char>((int64_t)scan_workspace((int64_t)n + 1));
+  const int64_t ocount = kClasses * order_blocks(n);
+  w.scan = a.take<char>((int64_t)scan_workspace(std::max<int64_t>((int64_t)n + 1, ocount + 1)));
   w.words = ceil_div(n, 32);
   w.bitmap = a.take<uint32_t>(kLargeBlocks * w.words);
   w.split = a.take<char>((int64_t)split_workspace(n));
+  w.ord_cnt = a.take<int32_t>(ocount);
+  w.ord_off = a.take<int64_t>(ocount + 1);
   return w;
 }
 
@@ -275,6 +289,39 @@ __global__ void __launch_bounds__(256) k_values(int32_t n, const int64_t* row_pt
   for (int64_t e = row_ptr[row] + lane; e < row_ptr[row + 1]; e += 64) val[e] = di * dinv[col_idx[e]];
 }
 
+// Length class of a row: 4 classes per power of two of the degree (its two bits below
+// the leading one), class 0 for the longest rows (degree >= 2^15.75).
+__device__ __forceinline__ int length_class(int32_t d) {
+  if (d < 4) return kClasses - 1 - d;
+  const int lg = 31 - __clz(d);
+  const int key = 4 * lg + ((d >> (lg - 2)) & 3);
+  return kClasses - 1 - (key < kClasses - 1 ? key : kClasses - 1);
+}
+
+__global__ void __launch_bounds__(kOrderBlock) k_order_count(int32_t n, const int32_t* deg, int32_t* cnt,
+                                                             int64_t nblk) {
+  __shared__ int32_t h[kClasses];
+  if (threadIdx.x < kClasses) h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t row = (int64_t)blockIdx.x * kOrderBlock + threadIdx.x;
+  if (row < n) atomicAdd(&h[length_class(deg[row])], 1);  // LDS integer counts
+  __syncthreads();
+  if (threadIdx.x < kClasses) cnt[(int64_t)threadIdx.x * nblk + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ void __launch_bounds__(kOrderBlock) k_order_place(int32_t n, const int32_t* deg, const int64_t* off,
+                                                             int64_t nblk, int32_t* order) {
+  __shared__ int32_t cls[kOrderBlock];
+  const int64_t row = (int64_t)blockIdx.x * kOrderBlock + threadIdx.x;
+  const int c = row < n ? length_class(deg[row]) : -1;
+  cls[threadIdx.x] = c;
+  __syncthreads();
+  if (row >= n) return;
+  int rank = 0;  // rows of the same class before this one in the block
+  for (int t = 0; t < (int)threadIdx.x; ++t) rank += cls[t] == c ? 1 : 0;
+  order[off[(int64_t)c * nblk + blockIdx.x] + rank] = (int32_t)row;
+}
+
 }  // namespace
 
 size_t build_csr_workspace(int32_t n, int64_t n_edges) {
@@ -342,6 +389,15 @@ gcn_status run_build_csr(int32_t n, int64_t n_edges, const int32_t* src, const i
     hipLaunchKernelGGL(k_values, dim3((unsigned)ceil_div(n, 4)), dim3(256), 0, s, n, g->row_ptr, g->col_idx,
                        g->dinv, g->val);
     GCN_TRY(check_launch("csr values"));
+  }
+  if (g->order && n > 0) {
+    const int64_t nblk = order_blocks(n);
+    hipLaunchKernelGGL(k_order_count, dim3((unsigned)nblk), dim3(kOrderBlock), 0, s, n, g->deg, w.ord_cnt, nblk);
+    GCN_TRY(check_launch("csr order count"));
+    GCN_TRY(launch_scan_i32(w.ord_cnt, kClasses * nblk, w.ord_off, w.scan, s));
+    hipLaunchKernelGGL(k_order_place, dim3((unsigned)nblk), dim3(kOrderBlock), 0, s, n, g->deg, w.ord_off, nblk,
+                       g->order);
+    GCN_TRY(check_launch("csr order place"));
   }
   g->split.order = nullptr;
   if (g->split.rows) GCN_TRY(build_split(g->row_ptr, n, &g->split, false, w.split, s));

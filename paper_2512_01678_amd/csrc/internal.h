@@ -100,6 +100,8 @@ struct AggParams {
   // AGG_RELU: optional bitmask of the output, bit c % 32 of word c / 32 of a row = 1[Z > 0]
   uint32_t* relu_bits;
   int64_t ld_relu_bits;    // words per row (>= ceil(w / 32))
+  // order in which the main kernel takes the rows (n entries), or NULL for 0 .. n-1
+  const int32_t* order;
 };
 // Words per row of a ReLU bitmask of width w.
 inline int64_t relu_bits_words(int32_t w) { return (w + 31) / 32; }

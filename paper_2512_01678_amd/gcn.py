@@ -50,7 +50,7 @@ class gcn_split(C.Structure):
 
 class gcn_graph(C.Structure):
     _fields_ = [("n", i32), ("nnz", i64), ("nnz_cap", i64), ("row_ptr", P), ("col_idx", P),
-                ("deg", P), ("dinv", P), ("val", P), ("split", gcn_split)]
+                ("deg", P), ("dinv", P), ("val", P), ("split", gcn_split), ("order", P)]
 
 
 class gcn_sparse_x(C.Structure):
@@ -199,21 +199,24 @@ class SplitPlan:
 class DeviceGraph:
     """A + I in CSR on the device (owning torch tensors), with its hub split plan."""
 
-    def __init__(self, n, row_ptr, col_idx, deg, dinv, val, nnz, plan: SplitPlan | None, split_c):
+    def __init__(self, n, row_ptr, col_idx, deg, dinv, val, nnz, plan: SplitPlan | None, split_c, order=None):
         self.n = n
         self.row_ptr, self.col_idx, self.deg, self.dinv, self.val = row_ptr, col_idx, deg, dinv, val
         self.nnz = nnz
         self.plan = plan
+        self.order = order  # rows in processing order (longest first), or None
         self.c = gcn_graph(n, nnz, col_idx.numel(), _ptr(row_ptr), _ptr(col_idx), _ptr(deg), _ptr(dinv),
-                           _ptr(val), split_c)
+                           _ptr(val), split_c, _ptr(order))
 
     @property
     def n_long(self):
         return self.c.split.n_long
 
 
-def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None, split: bool = True) -> DeviceGraph:
-    """gcn_build_csr on device int32 edge arrays; returns the graph (blocking)."""
+def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None, split: bool = True,
+              order: bool = True) -> DeviceGraph:
+    """gcn_build_csr on device int32 edge arrays; returns the graph (blocking).  order: also
+    build the row order of the aggregations (long rows first; results are the same)."""
     dev = src.device
     ne = src.numel()
     row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
@@ -222,11 +225,44 @@ def build_csr(n: int, src: torch.Tensor, dst: torch.Tensor, stream=None, split: 
     dinv = torch.empty(max(n, 1), dtype=torch.float32, device=dev)
     val = torch.empty(col.numel(), dtype=torch.float32, device=dev)
     plan = SplitPlan(2 * ne + n, dev, order=False) if split else None
+    ordv = torch.empty(max(n, 1), dtype=torch.int32, device=dev) if order else None
     g = gcn_graph(n, 0, col.numel(), _ptr(row_ptr), _ptr(col), _ptr(deg), _ptr(dinv), _ptr(val),
-                  plan.c if plan else gcn_split())
+                  plan.c if plan else gcn_split(), _ptr(ordv))
     _run_ws(_lib.gcn_build_csr, (n, ne, _ptr(src), _ptr(dst), C.byref(g)), (P(_stream(stream)),),
             "gcn_build_csr", None, dev)
-    return DeviceGraph(n, row_ptr, col, deg, dinv, val, g.nnz, plan, g.split)
+    return DeviceGraph(n, row_ptr, col, deg, dinv, val, g.nnz, plan, g.split, ordv)
+
+
+def tune_row_order(g: DeviceGraph, width: int, reps: int = 3) -> bool:
+    """Keep the graph's row order (long rows first) only where it makes the aggregation of
+    this width faster on this device: times gcn_aggregate both ways, twice each, and drops
+    the order when it does not win.  Every result is the same either way.  Returns whether
+    the order is kept."""
+    if g.order is None or g.n == 0:
+        return False
+    dev = g.row_ptr.device
+    M = torch.zeros((g.n, pitch(width)), dtype=torch.float32, device=dev)[:, :width]
+    Z = torch.empty_like(M)
+    ws = _Workspace()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(order_ptr):
+        g.c.order = order_ptr
+        aggregate(g, M, Z, ws=ws)
+        e0.record()
+        for _ in range(reps):
+            aggregate(g, M, Z, ws=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    on = min(timed(_ptr(g.order)), timed(_ptr(g.order)))
+    off = min(timed(None), timed(None))
+    keep = on < off
+    g.c.order = _ptr(g.order) if keep else None
+    if not keep:
+        g.order = None
+    return keep
 
 
 class SparseFeatures:

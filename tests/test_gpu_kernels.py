@@ -563,6 +563,88 @@ def test_softmax_layer_on_split_hubs(G, orc, hub_graph):
     np.testing.assert_allclose(host(out), Gr, rtol=0, atol=1e-4 * np.abs(Gr).max())
 
 
+def length_class(d):
+    """Processing class of a row of length d (0 first): 4 classes per power of two of d."""
+    d = np.asarray(d, np.int64)
+    lg = np.floor(np.log2(np.maximum(d, 1))).astype(np.int64)
+    key = np.where(d < 4, d, 4 * lg + ((d >> np.maximum(lg - 2, 0)) & 3))
+    return np.where(d < 4, 63 - d, 63 - np.minimum(key, 63))
+
+
+@pytest.mark.parametrize("case", ["hubs", "cora_like", "empty"])
+def test_row_order(G, orc, hub_graph, case):
+    """The row order of the aggregations: a permutation of the rows, by length class, longest
+    first, ties in row order; and every aggregation result (all epilogues, split hub rows,
+    the loss epilogue) is bit-identical with and without it."""
+    if case == "hubs":
+        og, dg = hub_graph
+        s = d = None
+    elif case == "cora_like":
+        wl = gs.WORKLOADS["cora_like"]
+        s, d = gs.make_graph(wl)
+        og, dg = orc.build_csr(wl.n, s, d), G.build_csr(wl.n, dev(s), dev(d))
+    else:
+        s = d = np.zeros(0, np.int32)
+        og, dg = orc.build_csr(300, s, d), G.build_csr(300, dev(s), dev(d))
+    n = og.n
+    order = host(dg.order)[:n]
+    np.testing.assert_array_equal(np.sort(order), np.arange(n))
+    cls = length_class(og.deg)[order]
+    key = cls.astype(np.int64) * (n + 1) + order
+    assert np.all(np.diff(key) > 0), "classes ascending (longest first), rows ascending within a class"
+    if case == "hubs":
+        e = host(dg.row_ptr)
+        s_ = np.repeat(np.arange(n, dtype=np.int32), np.diff(e))
+        d_ = host(dg.col_idx)[:og.nnz]
+    else:
+        s_, d_ = s, d
+    plain = G.build_csr(n, dev(s_), dev(d_), order=False)
+    assert plain.order is None and plain.nnz == dg.nnz
+    rng = np.random.default_rng(n)
+    for w in (7, 40, 256):
+        M = pitched(rng.standard_normal((n, w)).astype(np.float32), G.pitch(w))
+        b = dev(rng.standard_normal(w).astype(np.float32))
+        mask = pitched(rng.standard_normal((n, w)).astype(np.float32), G.pitch(w))
+        for epi in (G.EPI_NONE, G.EPI_RELU, G.EPI_MASK):
+            outs = []
+            for g in (dg, plain):
+                Z = pitched(np.zeros((n, w), np.float32), G.pitch(w))
+                G.aggregate(g, M, Z, bias=b, epi=epi, mask=mask if epi == G.EPI_MASK else None)
+                outs.append(host(Z))
+            np.testing.assert_array_equal(outs[0], outs[1])
+    # the loss epilogue (rows taken in groups of slots consecutive positions of the order)
+    H = pitched(np.maximum(rng.standard_normal((n, 64)), 0).astype(np.float32), 64)
+    W = dev((rng.standard_normal((64, 41)) / 8).astype(np.float32))
+    bb = dev((rng.standard_normal(41) * 0.1).astype(np.float32))
+    y = dev(rng.integers(0, 41, n).astype(np.int32))
+    L = G.make_layer(64, 41, 64, G.pitch(41), G.ACT_SOFTMAX_CE, 1)
+    res = []
+    for g in (dg, plain):
+        out = pitched(np.zeros((n, 41), np.float32), G.pitch(41))
+        logits = pitched(np.zeros((n, 41), np.float32), G.pitch(41))
+        loss = torch.zeros(1, device="cuda")
+        G.layer_fwd(g, L, H, None, W, bb, out, labels=y, loss=loss, logits=logits)
+        res.append((host(out), host(logits), host(loss)))
+    for a, c in zip(*res):
+        np.testing.assert_array_equal(a, c)
+
+
+def test_tune_row_order(G, orc):
+    """The tuner keeps or drops the order; either way the graph aggregates as before."""
+    wl = gs.WORKLOADS["cora_like"]
+    s, d = gs.make_graph(wl)
+    g = G.build_csr(wl.n, dev(s), dev(d))
+    rng = np.random.default_rng(3)
+    M = pitched(rng.standard_normal((wl.n, 40)).astype(np.float32), G.pitch(40))
+    before = pitched(np.zeros((wl.n, 40), np.float32), G.pitch(40))
+    G.aggregate(g, M, before)
+    kept = G.tune_row_order(g, 40)
+    assert kept == (g.order is not None) and (g.c.order is not None) == kept
+    after = pitched(np.zeros((wl.n, 40), np.float32), G.pitch(40))
+    G.aggregate(g, M, after)
+    np.testing.assert_array_equal(host(after), host(before))
+
+
 @pytest.mark.parametrize("fused", ["1", "0"])
 @pytest.mark.parametrize("fi,fo", [(128, 256), (48, 300)])
 def test_aggregate_first_layer_on_split_hubs(G, orc, hub_graph, fi, fo, fused, monkeypatch):
