@@ -571,14 +571,20 @@ def length_class(d):
     return np.where(d < 4, 63 - d, 63 - np.minimum(key, 63))
 
 
-@pytest.mark.parametrize("case", ["hubs", "cora_like", "empty"])
+@pytest.mark.parametrize("case", ["hubs", "dense", "cora_like", "empty"])
 def test_row_order(G, orc, hub_graph, case):
     """The row order of the aggregations: a permutation of the rows, by length class, longest
     first, ties in row order; and every aggregation result (all epilogues, split hub rows,
-    the loss epilogue) is bit-identical with and without it."""
+    the loss epilogue) is bit-identical with and without it.  The order is applied where an
+    average row gathers at least 4 KB: on the dense graph (about 67 entries per row) at every
+    width here, on the others at width 256."""
     if case == "hubs":
         og, dg = hub_graph
         s = d = None
+    elif case == "dense":
+        s, d = gs.chung_lu(6000, 200000, seed=8)
+        og, dg = orc.build_csr(6000, s, d), G.build_csr(6000, dev(s), dev(d))
+        assert og.nnz / og.n * 4 * 7 < 4096 < og.nnz / og.n * 4 * 40
     elif case == "cora_like":
         wl = gs.WORKLOADS["cora_like"]
         s, d = gs.make_graph(wl)
@@ -601,7 +607,7 @@ def test_row_order(G, orc, hub_graph, case):
     plain = G.build_csr(n, dev(s_), dev(d_), order=False)
     assert plain.order is None and plain.nnz == dg.nnz
     rng = np.random.default_rng(n)
-    for w in (7, 40, 256):
+    for w in (7, 16, 40, 256):
         M = pitched(rng.standard_normal((n, w)).astype(np.float32), G.pitch(w))
         b = dev(rng.standard_normal(w).astype(np.float32))
         mask = pitched(rng.standard_normal((n, w)).astype(np.float32), G.pitch(w))
