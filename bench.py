@@ -386,7 +386,8 @@ def main():
 
     # device memory during training (allocator high-water mark from the model's creation
     # on) against the O(N F) model: nothing may scale with nnz times a feature width
-    graph_bytes = 8 * (wl.n + 1) + 8 * g.col_idx.numel() + 8 * wl.n  # offsets, indices + values, deg + dinv
+    # offsets, indices + values, deg + dinv, and the row order when kept
+    graph_bytes = 8 * (wl.n + 1) + 8 * g.col_idx.numel() + 8 * wl.n + (4 * wl.n if g.order is not None else 0)
     x_bytes = 0 if sparse else 4 * wl.n * ld_x
     if sparse:  # X_csr (and X_csc): offsets, indices, values
         x_bytes = 8 * (wl.n + 1) + 8 * sx.col.numel()
