@@ -4,7 +4,8 @@ One training epoch (Algorithm 1 forward and backward, the softmax cross-entropy,
 of each full-size workload runs on the GPU as bench.py runs it: X at the bench's pitch,
 the density probe choosing the path (with the paper's tau = 4/5, so that the RMAT
 features at 10 % density take the sparse path too), the CSC view for a sparse first
-layer, every product at its automatic kernel choice.  Then the fp64 oracle
+layer, the row order of the aggregations kept or dropped by the same timing, every
+product at its automatic kernel choice.  Then the fp64 oracle
 checks, from the GPU's own layer inputs (unit parity, each element against its
 magnitude scale sum |terms|):
   * every hidden layer's output H_{l+1} (and the saved aggregate of an aggregate-first
@@ -75,6 +76,9 @@ class Run:
             self.og = orc.build_csr(n, s, d)
             self.dg = G.build_csr(n, torch.from_numpy(s).cuda(), torch.from_numpy(d).cuda())
             del s, d
+            # the row order, kept or dropped by the same setup-time timing as the bench's
+            kept = G.tune_row_order(self.dg, max(wl.widths[1:-1]) if len(wl.widths) > 2 else wl.widths[-1])
+            note(f"{wl.name}: row order {'kept' if kept else 'dropped'}")
         else:
             self.og, self.dg = graph
         assert self.dg.nnz == self.og.nnz
@@ -211,6 +215,8 @@ def rmat_graph(G, orc):
     s, d = gs.make_graph(wl)
     og = orc.build_csr(wl.n, s, d)
     dg = G.build_csr(wl.n, torch.from_numpy(s).cuda(), torch.from_numpy(d).cuda())
+    kept = G.tune_row_order(dg, max(wl.widths[1:-1]))
+    note(f"rmat21: row order {'kept' if kept else 'dropped'}")
     return og, dg
 
 
