@@ -17,7 +17,10 @@ magnitude scale sum |terms|):
     RMAT workloads 128 sampled rows of dW_0 = X^T Q_0, each a sum over all 2^21 nodes),
     the full bias gradient, and G_{l-1} on the sampled rows;
   * the Adam step of every parameter.
-The arxiv-shaped workload is checked on every row.  These sizes reach what the small
+The arxiv-shaped workload is checked on every row, also with the sum, mean and max
+aggregators on every layer (there the loss layer's gradient is held to what its logits'
+rounding allows per row: dG/dz moves G by at most 2/N of a logit's error, and the sum
+aggregator's logits reach thousands).  These sizes reach what the small
 tests cannot: operands above 2 GiB (H of the products-shaped graph is 2.5 GB, the RMAT
 features 34 GB), split-k weight gradients over 2.45 M rows, the row-panel products
 with 19,133 row panels, hub splitting on the RMAT graph and the row-chunk-tiled
@@ -66,8 +69,9 @@ def neighbours(og, rows):
 class Run:
     """One workload set up and trained for one epoch as bench.py does it."""
 
-    def __init__(self, G, orc, wl, graph=None):
+    def __init__(self, G, orc, wl, graph=None, agg=None):
         self.wl = wl
+        self.agg = agg  # None: the normalised GCN operator; else "sum", "mean" or "max" on every layer
         n = wl.n
         note(f"{wl.name}: drawing inputs")
         if graph is None:
@@ -99,7 +103,8 @@ class Run:
         self.sparse = info["mode"] == G.SPARSE
         note(f"{wl.name}: nnz(A+I) {self.og.nnz}, probe s = {info['sparsity']:.4f} -> "
              f"{'sparse' if self.sparse else 'dense'}; one GPU epoch")
-        self.m = G.Model(n, wl.widths, self.Ws, self.bs, x_sparse=self.sparse, ld_x=ld_x)
+        aggs = None if agg is None else [{"sum": G.AGG_SUM, "mean": G.AGG_MEAN, "max": G.AGG_MAX}[agg]] * (len(wl.widths) - 1)
+        self.m = G.Model(n, wl.widths, self.Ws, self.bs, x_sparse=self.sparse, ld_x=ld_x, aggs=aggs)
         self.m.epoch(self.dg, X=None if self.sparse else self.Xv, x=self.sx,
                      labels=torch.from_numpy(self.y).cuda())
         torch.cuda.synchronize()
@@ -236,3 +241,93 @@ def test_full_size_rmat(G, orc, rmat_graph, density):
     check_run(G, orc, run, rows, wl.name, x_cols=x_cols)
     del run
     torch.cuda.empty_cache()
+
+
+def check_run_agg(G, orc, run, what):
+    """check_run's unit parity on every row for a model whose layers all use run.agg (sum,
+    mean or max): each layer from the GPU's own input, the loss layer's gradient per row
+    within what its logits' rounding allows, every backward from the GPU's own G_l."""
+    wl, og, m, agg = run.wl, run.og, run.m, run.agg
+    n, L = wl.n, m.L
+    Ws = [w.astype(np.float64) for w in run.Ws]
+    bs = [b.astype(np.float64) for b in run.bs]
+    Hs = [run.x_rows(np.arange(n))] + [host(a, wl.widths[l + 1]) for l, a in enumerate(m.act)]
+    Ps = [None] * L  # max: the oracle's aggregate of each layer input (exact, as the GPU's)
+    args = [None] * L
+    flips = 0
+
+    def layer(l):
+        """Z_l and its magnitude scale from the GPU's own H_l."""
+        if agg == "max":
+            P, arg = orc.aggregate_max(og, Hs[l])
+            got_p = host(m.saved[l], wl.widths[l])
+            np.testing.assert_array_equal(got_p, P, err_msg=f"{what} max aggregate {l}")
+            ld = m.saved[l].stride(0)
+            # the maximisers follow the n rows of the saved aggregate in the same buffer
+            full = torch.as_strided(m.saved[l], (2 * n, ld), (ld, 1))
+            got_arg = full[n:].view(torch.int32)[:, :wl.widths[l]]
+            np.testing.assert_array_equal(host(got_arg), arg, err_msg=f"{what} argmax {l}")
+            Ps[l], args[l] = P, arg
+            return P @ Ws[l] + bs[l], np.abs(P) @ np.abs(Ws[l]) + np.abs(bs[l])
+        Z = orc.aggregate(og, Hs[l] @ Ws[l], bs[l], kind=agg)
+        mag = orc.aggregate(og, np.abs(Hs[l]) @ np.abs(Ws[l]), np.abs(bs[l]), kind=agg)
+        if m.saved[l] is not None:
+            P, pmag = orc.aggregate(og, Hs[l], kind=agg, want_mag=True)
+            assert_mag_close(host(m.saved[l], wl.widths[l]), P, pmag, f"{what} saved aggregate {l}")
+        return Z, mag
+
+    for l in range(L - 1):
+        note(f"{what}: forward layer {l}")
+        Z, mag = layer(l)
+        got = Hs[l + 1]
+        flips += relu_flips(got > 0, Z, mag, f"{what} H_{l + 1}")
+        assert_mag_close(got, np.maximum(Z, 0), mag, f"{what} H_{l + 1}")
+    note(f"{what}: loss layer")
+    Zl, zmag = layer(L - 1)
+    lo, Gl, _ = orc.softmax_ce(Zl, run.y)
+    assert float(m.loss.cpu()[0]) == pytest.approx(lo, rel=1e-4), f"{what} loss"
+    # dG/dz has row sums of absolute values <= 2 / N, so a logit error within 1e-4 of its
+    # scale moves G by at most 2e-4 / N times the row's largest logit scale
+    gg = host(m.grad[L - 1], wl.widths[L])
+    bound = 2e-4 * zmag.max(axis=1, keepdims=True) / n + 1e-7 / n
+    worst = float((np.abs(gg - Gl) / bound).max())
+    assert worst <= 1.0, f"{what} G_{L - 1}: error {worst:.3f} of its per-row bound"
+    del Zl, Gl
+    for l in range(L - 1, -1, -1):
+        note(f"{what}: backward layer {l}")
+        Gg = host(m.grad[l], wl.widths[l + 1])
+        assert_mag_close(host(m.db[l][None, :])[0], Gg.sum(axis=0), np.abs(Gg).sum(axis=0), f"{what} db_{l}")
+        if agg == "max":
+            P = Ps[l]
+            assert_mag_close(host(m.dW[l]), P.T @ Gg, np.abs(P).T @ np.abs(Gg), f"{what} dW_{l}")
+            if l > 0:
+                dP = Gg @ Ws[l].T
+                dPm = np.abs(Gg) @ np.abs(Ws[l]).T
+                ref = orc.aggregate_max_backward(og, dP, args[l]) * (Hs[l] > 0)
+                mag = orc.aggregate_max_backward(og, dPm, args[l])
+                assert_mag_close(host(m.grad[l - 1], wl.widths[l]), ref, mag, f"{what} G_{l - 1}")
+        else:
+            Q, aQ = orc.aggregate(og, Gg, kind="mean_t" if agg == "mean" else agg, want_mag=True)
+            assert_mag_close(host(m.dW[l]), Hs[l].T @ Q, np.abs(Hs[l]).T @ aQ, f"{what} dW_{l}")
+            if l > 0:
+                ref = (Q @ Ws[l].T) * (Hs[l] > 0)
+                assert_mag_close(host(m.grad[l - 1], wl.widths[l]), ref, aQ @ np.abs(Ws[l]).T, f"{what} G_{l - 1}")
+    for l in range(L):
+        for nm, gnm, p0 in (("W", "dW", Ws[l]), ("b", "db", bs[l])):
+            g = host(getattr(m, gnm)[l][None] if nm == "b" else getattr(m, gnm)[l])
+            g = g[0] if nm == "b" else g
+            want, _, _ = orc.adam(p0, g, np.zeros_like(p0), np.zeros_like(p0), 1)
+            got = host(getattr(m, nm)[l][None] if nm == "b" else getattr(m, nm)[l])
+            got = got[0] if nm == "b" else got
+            assert_mag_close(got, want, np.abs(p0) + 0.01, f"{what} Adam {nm}_{l}", rtol=1e-5)
+    note(f"{what}: passed ({flips} ReLU flips near zero in total)")
+
+
+@pytest.mark.parametrize("agg", ["sum", "mean", "max"])
+def test_full_size_arxiv_like_aggregators(G, orc, agg):
+    """The full arxiv-shaped workload with every layer on the sum, mean or max aggregator
+    (`bench.py --workload arxiv_like --agg ...`), checked on every row."""
+    run = Run(G, orc, gs.WORKLOADS["arxiv_like"], agg=agg)
+    if agg == "max":
+        assert run.m.orders() == [G.AGGREGATE_FIRST] * 3
+    check_run_agg(G, orc, run, f"arxiv_like {agg}")
