@@ -69,7 +69,7 @@ def neighbours(og, rows):
 class Run:
     """One workload set up and trained for one epoch as bench.py does it."""
 
-    def __init__(self, G, orc, wl, graph=None, agg=None):
+    def __init__(self, G, orc, wl, graph=None, agg=None, csc=True):
         self.wl = wl
         self.agg = agg  # None: the normalised GCN operator; else "sum", "mean" or "max" on every layer
         n = wl.n
@@ -99,7 +99,7 @@ class Run:
         else:
             self.Xv.copy_(torch.from_numpy(self.X).cuda())
         torch.cuda.synchronize()
-        info, self.sx = G.feature_stats(self.Xv, tau=(4, 5), force_mode=-1, csc=True)
+        info, self.sx = G.feature_stats(self.Xv, tau=(4, 5), force_mode=-1, csc=csc)
         self.sparse = info["mode"] == G.SPARSE
         note(f"{wl.name}: nnz(A+I) {self.og.nnz}, probe s = {info['sparsity']:.4f} -> "
              f"{'sparse' if self.sparse else 'dense'}; one GPU epoch")
@@ -239,6 +239,21 @@ def test_full_size_rmat(G, orc, rmat_graph, density):
     note(f"{wl.name}: {rows.size} sampled rows, {n_hubs} hub rows above {SPLIT_MIN} entries")
     x_cols = np.unique(np.concatenate([rng.integers(0, wl.f, 120), [0, 1, wl.f - 2, wl.f - 1]])).astype(np.int64)
     check_run(G, orc, run, rows, wl.name, x_cols=x_cols)
+    del run
+    torch.cuda.empty_cache()
+
+
+def test_full_size_rmat_atomic_transpose(G, orc, rmat_graph):
+    """The sparse path without the CSC view (`bench.py --csc off`): dW_0 = X^T Q_0 by atomic
+    adds from X_csr rows, at the 1 % RMAT workload's full size; its rounding order varies
+    from run to run, the result stays within the magnitude bar."""
+    wl = gs.WORKLOADS["rmat21_p0.01"]
+    run = Run(G, orc, wl, graph=rmat_graph, csc=False)
+    assert run.sparse and run.sx.col_ptr is None
+    rng = np.random.default_rng(2)
+    rows, n_hubs = sample_rows(run.og, 400)
+    x_cols = np.unique(np.concatenate([rng.integers(0, wl.f, 120), [0, wl.f - 1]])).astype(np.int64)
+    check_run(G, orc, run, rows, wl.name + " (atomic X^T Q)", x_cols=x_cols)
     del run
     torch.cuda.empty_cache()
 
